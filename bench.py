@@ -1,0 +1,260 @@
+"""Benchmark of one dense-layer training step (forward, gradient subgraph,
+SGD update) through libtfdense on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Prints ONE JSON line. The headline workload is the 4-layer, 4096-wide MLP
+with 16-bit activations/weights, fp32 accumulation and fp32 master weights,
+batch 16384 ("wide4096x4-bf16"); its fp32 twin at batch 8192
+("wide4096x4-f32") is timed in the same run and reported under "also".
+
+Timing: every step starts from the same Variables (a stream-ordered restore
+before the step's start event), so each timed step is exactly the computation
+the parity tests check. ms_per_step is the mean of the per-step HIP event
+intervals on the launch stream; the host-side bracket (synchronize on both
+sides of the K steps, restores included) is reported as wall_ms_per_step.
+Throughput counts the step's GEMM FLOPs, sum of 2*m*n*k.
+The cpu_baseline leg times the oracle (float64 numpy) on a row slice of the
+same workload on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "TFLOP/s per dense-layer fwd+bwd+SGD step; % of MI355X MFMA peak"
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks (256 CUs x 2.4 GHz)
+HBM_PEAK_GBS = 8000.0
+PRIMARY = "wide4096x4-bf16"
+SECONDARY = "wide4096x4-f32"
+
+
+def _op_kind(name: str) -> str:
+    for p in ("fwd", "dx", "dw", "relugrad", "sgd", "loss"):
+        if name.startswith(p):
+            return p
+    return name
+
+
+def time_workload(name: str, steps: int, warmup: int):
+    import torch
+
+    from paper_1603_04467_amd import workloads
+    from paper_1603_04467_amd.step import DenseStep
+
+    w = workloads.workload(name)
+    inp = workloads.generate(w, seed=0)
+    s = DenseStep(w, inp)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(warmup):
+        s.restore()
+        s.run()
+    torch.cuda.synchronize()
+
+    # per-step and per-op events, recorded on the launch stream
+    step_ev = []
+    op_ev = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        s.restore()
+        marks = []
+
+        def mark(tag, marks=marks):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            marks.append((tag, e))
+
+        s.run(mark=mark)
+        step_ev.append((marks[0][1], marks[-1][1]))
+        op_ev.append(marks)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+
+    step_ms = [a.elapsed_time(b) for a, b in step_ev]
+    per_op = {}
+    for marks in op_ev:
+        for (tag, e0), (_, e1) in zip(marks[:-1], marks[1:]):
+            per_op.setdefault(tag, []).append(e0.elapsed_time(e1))
+    ms = float(np.mean(step_ms))
+    flops = w.flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+
+    # per-op summary: mean ms, and FLOP/s or bytes/s against the roofline
+    gemm_shapes = w.gemm_shapes()
+    L = w.layers
+    eb = 2 if w.act == "bf16" else 4
+    N = w.batch
+    ops = {}
+    for tag, v in per_op.items():
+        kind = _op_kind(tag)
+        l = int(tag[len(kind):]) if tag[len(kind):].isdigit() else None
+        d = {"ms": float(np.mean(v))}
+        if kind in ("fwd", "dx", "dw"):
+            if kind == "fwd":
+                m, n, k, lay = gemm_shapes[l - 1]
+            else:
+                idx = L + 2 * (L - l) + (0 if kind == "dx" else 1)
+                m, n, k, lay = gemm_shapes[idx]
+            f = 2 * m * n * k
+            d.update(layout=lay, shape=[m, n, k], flops=f, tflops=f / (d["ms"] * 1e-3) / 1e12)
+        elif kind == "relugrad":
+            M = w.dims[l]
+            byt = (3 * N * M * eb if w.relus[l - 1] else N * M * eb) + 4 * M
+            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
+        elif kind == "sgd":
+            K, M = w.dims[l - 1], w.dims[l]
+            byt = K * M * (12 + (2 if w.masters else 0)) + 12 * M
+            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
+        elif kind == "loss":
+            byt = 3 * N * w.dims[-1] * eb
+            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
+        ops[tag] = d
+
+    # dominant kernel: the GEMM layout with the most total time
+    by_layout = {}
+    for tag, d in ops.items():
+        if "layout" in d:
+            by_layout.setdefault(d["layout"], []).append(d)
+    dom_layout, dom = max(by_layout.items(), key=lambda kv: sum(x["ms"] for x in kv[1]))
+    dom_ms = float(np.mean([x["ms"] for x in dom]))
+    dom_flops = dom[0]["flops"]
+    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.act]
+    return {
+        "workload": w,
+        "ms": ms,
+        "wall_ms": wall,
+        "tflops": tflops,
+        "pct_peak": 100.0 * tflops / peak,
+        "ops": ops,
+        "roofline": {
+            "bound": "mfma",
+            "kernel": f"gemm_{dom_layout}_{w.act}",
+            "shape": dom[0]["shape"],
+            "achieved": achieved,
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": achieved / peak,
+            "traffic": None,
+        },
+        "loss": float(s.loss.item()),
+    }
+
+
+def cpu_baseline(name: str, rows: int):
+    """Time the oracle's step on the first `rows` batch rows of the workload."""
+    import oracle
+    from paper_1603_04467_amd import workloads
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    w = workloads.workload(name)
+    inp = workloads.generate(w, seed=0)
+    conv = oracle.bf16_bits_to_f64 if w.act == "bf16" else (lambda a: a.astype(np.float64))
+    x = conv(inp["x"])[:rows]
+    t = None if inp["target"] is None else conv(inp["target"])[:rows]
+    ws = [conv(a) for a in inp["weights"]]
+    ms_ = None if inp["masters"] is None else [a.astype(np.float64) for a in inp["masters"]]
+    bs = [a.astype(np.float64) for a in inp["biases"]]
+    t0 = time.perf_counter()
+    oracle.dense_step(x, ws, bs, list(w.relus), act=w.act, target=t, lr=w.lr, masters=ms_, update=w.update)
+    dt = time.perf_counter() - t0
+    flops = w.scaled(batch=rows).flops()
+    return {
+        "value": flops / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{name}: one full step on batch rows 0..{rows - 1} of {w.batch} "
+                  f"({flops / 1e12:.3f} TFLOP in {dt:.1f} s, float64 numpy)",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=PRIMARY)
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=1024)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the data-parallel sharding is a design note only).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "no GPU visible"
+    torch.cuda.set_device(0)
+
+    print(f"bench: timing {args.workload} ({args.steps} steps, {args.warmup} warm-up)", file=sys.stderr, flush=True)
+    r = time_workload(args.workload, args.steps, args.warmup)
+    w = r["workload"]
+    out = {
+        "metric": METRIC,
+        "value": round(r["tflops"], 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["ms"], 4),
+        "wall_ms_per_step": round(r["wall_ms"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.act,
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": w.batch,
+            "dims": list(w.dims),
+            "relus": list(w.relus),
+            "storage": w.act,
+            "accumulate": "f32",
+            "master_weights": "f32" if (w.masters or w.act == "f32") else None,
+            "lr": w.lr,
+            "gemm_flops_per_step": w.flops(),
+        },
+        "pct_mfma_peak": round(r["pct_peak"], 2),
+        "roofline": r["roofline"],
+        "per_op_ms": {k: round(v["ms"], 4) for k, v in r["ops"].items()},
+        "loss": r["loss"],
+    }
+    if not args.no_secondary and args.workload == PRIMARY:
+        print(f"bench: timing {SECONDARY}", file=sys.stderr, flush=True)
+        r2 = time_workload(SECONDARY, args.steps, args.warmup)
+        out["also"] = {
+            "workload": SECONDARY,
+            "value": round(r2["tflops"], 3),
+            "unit": "TFLOP/s",
+            "ms_per_step": round(r2["ms"], 4),
+            "pct_mfma_peak": round(r2["pct_peak"], 2),
+            "roofline": r2["roofline"],
+            "per_op_ms": {k: round(v["ms"], 4) for k, v in r2["ops"].items()},
+        }
+    if not args.no_cpu_baseline:
+        print(f"bench: timing the oracle on {args.cpu_rows} rows", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

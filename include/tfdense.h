@@ -1,0 +1,182 @@
+/*
+ * libtfdense — the dense-layer training step of the TensorFlow white paper
+ * (Abadi et al., 2015) as hand-written HIP kernels for AMD CDNA4 (gfx950).
+ *
+ * The paper's canonical example (Figure 1) trains Relu(W x + b). Its graph
+ * uses the ops MatMul, Add and ReLU (section 2, Table 1); automatic
+ * differentiation (section 4.1) adds their gradient functions; the
+ * parameters live in Variables that the step updates in place (section 2,
+ * "Variables"). This library exports one call per op on that path.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Matrices are 2-D, row-major. A leading dimension ("ld") is the distance
+ *    in elements between consecutive rows and must be >= the row length.
+ *  - Element types: TFD_F32 (IEEE binary32) and TFD_BF16 (the 16-bit float
+ *    of section 5.5: binary32 with 16 fewer mantissa bits). Products are
+ *    accumulated in fp32. Values stored as TFD_BF16 are rounded to nearest
+ *    even. Biases, bias gradients and Variables are always fp32.
+ *  - Pointers are device pointers unless stated otherwise. The caller owns
+ *    every buffer; the library allocates no device memory, keeps no state
+ *    between calls and never synchronises. Scratch memory is passed in as a
+ *    "workspace" sized by the matching *_workspace_size call.
+ *  - Every call enqueues its kernels on `stream` (a hipStream_t passed as
+ *    void*; NULL is the null stream) and returns. Stream order is the only
+ *    ordering: it plays the role of the paper's control dependencies
+ *    (section 2), e.g. a weight gradient that must read W before the update
+ *    writes it is simply enqueued first.
+ *  - Errors: a call returns TFD_OK, or an error status before enqueuing
+ *    anything (TFD_EINVAL: a NULL pointer with a non-zero size, a negative
+ *    size, a leading dimension smaller than the row, a workspace too small,
+ *    an aliasing the call forbids; TFD_EUNSUPPORTED: an element-type
+ *    combination the call does not implement; TFD_EHIP: the HIP runtime
+ *    rejected a launch). tfd_last_error() then holds a message (per host
+ *    thread). No C++ exception crosses this interface. A fault inside a
+ *    kernel surfaces at the caller's next synchronisation.
+ *  - Sizes of zero are valid and enqueue nothing (except where stated).
+ */
+#ifndef TFDENSE_H
+#define TFDENSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TFD_ABI_VERSION 1
+
+#if defined(__GNUC__)
+#define TFD_API __attribute__((visibility("default")))
+#else
+#define TFD_API
+#endif
+
+typedef enum tfd_status {
+  TFD_OK = 0,
+  TFD_EINVAL = 1,
+  TFD_EUNSUPPORTED = 2,
+  TFD_EHIP = 3
+} tfd_status;
+
+typedef enum tfd_dtype { TFD_F32 = 0, TFD_BF16 = 1 } tfd_dtype;
+
+/* What the MatMul producer applies to the fp32 accumulator before the
+ * single rounding to the output type. */
+typedef enum tfd_epilogue {
+  TFD_EPI_NONE = 0,      /* C = op(A) op(B)                                 */
+  TFD_EPI_BIAS = 1,      /* C = op(A) op(B) + 1 bias^T        (Add, Fig. 1) */
+  TFD_EPI_BIAS_RELU = 2  /* C = Relu(op(A) op(B) + 1 bias^T)  (Relu(Wx+b))  */
+} tfd_epilogue;
+
+TFD_API int tfd_abi_version(void);
+TFD_API const char* tfd_status_string(tfd_status status);
+/* Message of the last failed call on this host thread ("" if none). */
+TFD_API const char* tfd_last_error(void);
+
+/*
+ * MatMul (section 2, Table 1) with the op's transpose attributes, fused with
+ * the broadcast bias Add and the ReLU of Figure 1:
+ *   C[m x n] = epilogue( op(A)[m x k] * op(B)[k x n] ),
+ *   op(A) = A^T if transpose_a (A stored k x m, lda >= m) else A (m x k, lda >= k),
+ *   op(B) = B^T if transpose_b (B stored n x k, ldb >= k) else B (k x n, ldb >= n).
+ * The three layouts of one dense layer's step: forward Y = X W (NN), input
+ * gradient dX = dY W^T (transpose_b = 1) and weight gradient dW = X^T dY
+ * (transpose_a = 1).
+ * Types: (a, b, c) in {(F32, F32, F32), (BF16, BF16, BF16), (BF16, BF16, F32)};
+ * fp32 accumulation. bias is fp32[n] (may be NULL only with TFD_EPI_NONE).
+ * ReLU keeps values > 0 and writes +0 otherwise. k = 0 gives
+ * C = epilogue(0). C must not overlap A, B or bias. Returns TFD_EUNSUPPORTED
+ * for other type combinations and for transpose_a && transpose_b.
+ */
+TFD_API tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                      const void* a, int64_t lda, tfd_dtype a_type,
+                      const void* b, int64_t ldb, tfd_dtype b_type,
+                      void* c, int64_t ldc, tfd_dtype c_type,
+                      const float* bias, tfd_epilogue epilogue, void* stream);
+
+/*
+ * BiasAdd, the broadcast Add of Figure 1 on its own:
+ *   out[r, c] = value[r, c] + bias[c], rows x cols, contiguous (ld = cols).
+ * value/out in `type` (fp32 arithmetic, one rounding); bias fp32[cols].
+ * out may equal value.
+ */
+TFD_API tfd_status tfd_bias_add(const void* value, const float* bias, void* out,
+                        int64_t rows, int64_t cols, tfd_dtype type, void* stream);
+
+/*
+ * ReLU (Table 1): activations[i] = features[i] > 0 ? features[i] : +0,
+ * `count` contiguous elements of `type`. activations may equal features.
+ */
+TFD_API tfd_status tfd_relu(const void* features, void* activations, int64_t count,
+                    tfd_dtype type, void* stream);
+
+/*
+ * ReluGrad, the gradient function of ReLU (section 4.1):
+ *   backprops[i] = features[i] > 0 ? gradients[i] : +0,
+ * with `features` the stored forward output of the Relu. backprops may
+ * equal gradients.
+ */
+TFD_API tfd_status tfd_relu_grad(const void* gradients, const void* features, void* backprops,
+                         int64_t count, tfd_dtype type, void* stream);
+
+/* Workspace bytes that tfd_bias_add_grad and tfd_relu_grad_bias_add_grad
+ * need for a rows x cols input. */
+TFD_API size_t tfd_reduction_workspace_size(int64_t rows, int64_t cols, tfd_dtype type);
+
+/*
+ * BiasAddGrad, the gradient of the broadcast Add with respect to the bias
+ * (the db of section 4.1's tf.gradients(C, [b, W, x])):
+ *   bias_grad[c] = sum_r out_backprop[r, c]   (fp32 out, fp32 partial sums).
+ * The summation order is fixed by (rows, cols), so repeated calls give
+ * identical bits. rows = 0 writes zeros.
+ */
+TFD_API tfd_status tfd_bias_add_grad(const void* out_backprop, float* bias_grad,
+                             int64_t rows, int64_t cols, tfd_dtype type,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ReluGrad fused with BiasAddGrad in one pass over the gradient:
+ *   d = features[r, c] > 0 ? gradients[r, c] : +0,
+ *   backprops[r, c] = d (skipped when backprops is NULL),
+ *   bias_grad[c] = sum_r d.
+ * features == NULL means an identity layer (d = gradients). backprops must
+ * not overlap gradients or features. Deterministic like tfd_bias_add_grad.
+ */
+TFD_API tfd_status tfd_relu_grad_bias_add_grad(const void* gradients, const void* features,
+                                       void* backprops, float* bias_grad,
+                                       int64_t rows, int64_t cols, tfd_dtype type,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream);
+
+/* Workspace bytes that tfd_l2_loss_grad needs for `count` elements. */
+TFD_API size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type);
+
+/*
+ * Cost head: the squared error L = 1/2 sum_i (output[i] - target[i])^2 and
+ * its gradient grad[i] = output[i] - target[i] (the exact difference rounded
+ * once to `type`). target == NULL means 0 (L = 1/2 sum output^2,
+ * grad = output). `loss` is a device double, written with a fixed summation
+ * order (float64 partial sums of the fp32 squares). grad may equal output.
+ */
+TFD_API tfd_status tfd_l2_loss_grad(const void* output, const void* target, void* grad, double* loss,
+                            int64_t count, tfd_dtype type,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ApplyGradientDescent on an fp32 Variable (section 2 "Variables"; the SGD
+ * step of section 4.1), in place:
+ *   var[i] = fma(-alpha, delta[i], var[i])   (one rounding),
+ * and, when var_bf16 != NULL, var_bf16[i] = the updated var[i] rounded to
+ * nearest even in the 16-bit format (the operand copy of 16-bit GEMMs).
+ * delta must not overlap var.
+ */
+TFD_API tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delta,
+                                      int64_t count, uint16_t* var_bf16, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TFDENSE_H */

@@ -1,0 +1,236 @@
+// C ABI of libtfdense: argument validation and dispatch to the kernels.
+// The contract of every entry point is documented in include/tfdense.h.
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/tfdense.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tfd_status fail(tfd_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+tfd_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return TFD_OK;
+  return fail(TFD_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool valid_dtype(tfd_dtype t) { return t == TFD_F32 || t == TFD_BF16; }
+int elem_bytes(tfd_dtype t) { return t == TFD_BF16 ? 2 : 4; }
+
+// Byte ranges [p, p + bytes) overlap?
+bool overlaps(const void* p, size_t pb, const void* q, size_t qb) {
+  if (!p || !q || pb == 0 || qb == 0) return false;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+  return a < b + qb && b < a + pb;
+}
+
+// Extent in bytes of a rows x cols matrix with leading dimension ld.
+size_t span(int64_t rows, int64_t cols, int64_t ld, int eb) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return (size_t)((rows - 1) * ld + cols) * (size_t)eb;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tfd_abi_version(void) { return TFD_ABI_VERSION; }
+
+const char* tfd_status_string(tfd_status s) {
+  switch (s) {
+    case TFD_OK: return "ok";
+    case TFD_EINVAL: return "invalid argument";
+    case TFD_EUNSUPPORTED: return "unsupported";
+    case TFD_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* tfd_last_error(void) { return g_err; }
+
+tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                      const void* a, int64_t lda, tfd_dtype a_type,
+                      const void* b, int64_t ldb, tfd_dtype b_type,
+                      void* c, int64_t ldc, tfd_dtype c_type,
+                      const float* bias, tfd_epilogue epilogue, void* stream) {
+  g_err[0] = 0;
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "tfd_matmul: negative size m=%lld n=%lld k=%lld", (long long)m, (long long)n, (long long)k);
+  if (!valid_dtype(a_type) || !valid_dtype(b_type) || !valid_dtype(c_type))
+    return fail(TFD_EINVAL, "tfd_matmul: unknown element type");
+  if (epilogue != TFD_EPI_NONE && epilogue != TFD_EPI_BIAS && epilogue != TFD_EPI_BIAS_RELU)
+    return fail(TFD_EINVAL, "tfd_matmul: unknown epilogue %d", (int)epilogue);
+  if (transpose_a && transpose_b)
+    return fail(TFD_EUNSUPPORTED, "tfd_matmul: transpose_a and transpose_b together are not implemented");
+  if (a_type != b_type || (a_type == TFD_F32 && c_type != TFD_F32))
+    return fail(TFD_EUNSUPPORTED, "tfd_matmul: element types (a=%d, b=%d, c=%d) not implemented", a_type, b_type, c_type);
+  // The kernels index with 32-bit tile coordinates.
+  if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30))
+    return fail(TFD_EUNSUPPORTED, "tfd_matmul: dimension above 2^30");
+  const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
+  const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
+  if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1) || ldc < (n > 0 ? n : 1))
+    return fail(TFD_EINVAL, "tfd_matmul: leading dimension smaller than the row (lda=%lld ldb=%lld ldc=%lld)", (long long)lda, (long long)ldb, (long long)ldc);
+  if (m == 0 || n == 0) return TFD_OK;
+  if (!c) return fail(TFD_EINVAL, "tfd_matmul: c is NULL");
+  if (k > 0 && (!a || !b)) return fail(TFD_EINVAL, "tfd_matmul: a or b is NULL");
+  if (epilogue != TFD_EPI_NONE && !bias) return fail(TFD_EINVAL, "tfd_matmul: the bias epilogue needs a bias");
+  const int ab = elem_bytes(a_type), cb = elem_bytes(c_type);
+  const size_t c_span = span(m, n, ldc, cb);
+  if (overlaps(c, c_span, a, span(a_rows, a_cols, lda, ab)) ||
+      overlaps(c, c_span, b, span(b_rows, b_cols, ldb, ab)) ||
+      (epilogue != TFD_EPI_NONE && overlaps(c, c_span, bias, (size_t)n * 4)))
+    return fail(TFD_EINVAL, "tfd_matmul: c overlaps an input");
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.a = a;
+  d.lda = lda;
+  d.b = b;
+  d.ldb = ldb;
+  d.c = c;
+  d.ldc = ldc;
+  d.in_bf16 = a_type == TFD_BF16;
+  d.out_bf16 = c_type == TFD_BF16;
+  d.bias = bias;
+  d.epi = (int)epilogue;
+  return hip_status(tfd::launch_gemm(d, as_stream(stream)), "tfd_matmul launch");
+}
+
+tfd_status tfd_bias_add(const void* value, const float* bias, void* out, int64_t rows, int64_t cols,
+                        tfd_dtype type, void* stream) {
+  g_err[0] = 0;
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "tfd_bias_add: negative size");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_bias_add: unknown element type");
+  if (rows == 0 || cols == 0) return TFD_OK;
+  if (!value || !bias || !out) return fail(TFD_EINVAL, "tfd_bias_add: NULL pointer");
+  const size_t bytes = (size_t)(rows * cols) * elem_bytes(type);
+  if (value != out && overlaps(value, bytes, out, bytes))
+    return fail(TFD_EINVAL, "tfd_bias_add: out partially overlaps value");
+  if (overlaps(bias, (size_t)cols * 4, out, bytes)) return fail(TFD_EINVAL, "tfd_bias_add: out overlaps bias");
+  return hip_status(tfd::launch_bias_add(value, bias, out, rows, cols, type == TFD_BF16, as_stream(stream)),
+                    "tfd_bias_add launch");
+}
+
+tfd_status tfd_relu(const void* features, void* activations, int64_t count, tfd_dtype type, void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_relu: negative count");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_relu: unknown element type");
+  if (count == 0) return TFD_OK;
+  if (!features || !activations) return fail(TFD_EINVAL, "tfd_relu: NULL pointer");
+  const size_t bytes = (size_t)count * elem_bytes(type);
+  if (features != activations && overlaps(features, bytes, activations, bytes))
+    return fail(TFD_EINVAL, "tfd_relu: activations partially overlap features");
+  return hip_status(tfd::launch_relu(features, activations, count, type == TFD_BF16, as_stream(stream)),
+                    "tfd_relu launch");
+}
+
+tfd_status tfd_relu_grad(const void* gradients, const void* features, void* backprops, int64_t count,
+                         tfd_dtype type, void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_relu_grad: negative count");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_relu_grad: unknown element type");
+  if (count == 0) return TFD_OK;
+  if (!gradients || !features || !backprops) return fail(TFD_EINVAL, "tfd_relu_grad: NULL pointer");
+  const size_t bytes = (size_t)count * elem_bytes(type);
+  if ((backprops != gradients && overlaps(backprops, bytes, gradients, bytes)) ||
+      overlaps(backprops, bytes, features, bytes))
+    return fail(TFD_EINVAL, "tfd_relu_grad: backprops overlaps features or part of gradients");
+  return hip_status(tfd::launch_relu_grad(gradients, features, backprops, count, type == TFD_BF16,
+                                          as_stream(stream)),
+                    "tfd_relu_grad launch");
+}
+
+size_t tfd_reduction_workspace_size(int64_t rows, int64_t cols, tfd_dtype type) {
+  if (rows < 0 || cols <= 0 || !valid_dtype(type)) return 0;
+  return tfd::reduction_ws_bytes(rows, cols, type == TFD_BF16);
+}
+
+tfd_status tfd_relu_grad_bias_add_grad(const void* gradients, const void* features, void* backprops,
+                                       float* bias_grad, int64_t rows, int64_t cols, tfd_dtype type,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: negative size");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: unknown element type");
+  if (cols == 0) return TFD_OK;
+  if (!bias_grad) return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: bias_grad is NULL");
+  if (rows > 0 && !gradients) return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: gradients is NULL");
+  const size_t need = tfd::reduction_ws_bytes(rows, cols, type == TFD_BF16);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  const size_t bytes = (size_t)(rows * cols) * elem_bytes(type);
+  if (overlaps(backprops, bytes, gradients, bytes) || overlaps(backprops, bytes, features, bytes) ||
+      overlaps(workspace, need, gradients, bytes) || overlaps(workspace, need, backprops, bytes) ||
+      overlaps(bias_grad, (size_t)cols * 4, backprops, bytes) || overlaps(bias_grad, (size_t)cols * 4, workspace, need))
+    return fail(TFD_EINVAL, "tfd_relu_grad_bias_add_grad: overlapping buffers");
+  return hip_status(tfd::launch_relu_grad_bias_add_grad(gradients, features, backprops, bias_grad, rows, cols,
+                                                        type == TFD_BF16, workspace, as_stream(stream)),
+                    "tfd_relu_grad_bias_add_grad launch");
+}
+
+tfd_status tfd_bias_add_grad(const void* out_backprop, float* bias_grad, int64_t rows, int64_t cols,
+                             tfd_dtype type, void* workspace, size_t workspace_bytes, void* stream) {
+  tfd_status st = tfd_relu_grad_bias_add_grad(out_backprop, nullptr, nullptr, bias_grad, rows, cols, type,
+                                              workspace, workspace_bytes, stream);
+  if (st != TFD_OK && strncmp(g_err, "tfd_relu_grad_bias_add_grad", 27) == 0) {
+    char tmp[512];
+    snprintf(tmp, sizeof(tmp), "tfd_bias_add_grad%s", g_err + 27);
+    memcpy(g_err, tmp, sizeof(tmp));
+  }
+  return st;
+}
+
+size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type) {
+  if (count < 0 || !valid_dtype(type)) return 0;
+  return tfd::loss_ws_bytes(count, type == TFD_BF16);
+}
+
+tfd_status tfd_l2_loss_grad(const void* output, const void* target, void* grad, double* loss, int64_t count,
+                            tfd_dtype type, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_l2_loss_grad: negative count");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_l2_loss_grad: unknown element type");
+  if (!loss) return fail(TFD_EINVAL, "tfd_l2_loss_grad: loss is NULL");
+  if (count > 0 && (!output || !grad)) return fail(TFD_EINVAL, "tfd_l2_loss_grad: NULL pointer");
+  const size_t need = tfd::loss_ws_bytes(count, type == TFD_BF16);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "tfd_l2_loss_grad: workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  const size_t bytes = (size_t)count * elem_bytes(type);
+  if ((grad != output && overlaps(grad, bytes, output, bytes)) || overlaps(grad, bytes, target, bytes) ||
+      overlaps(workspace, need, grad, bytes) || overlaps(loss, 8, grad, bytes) || overlaps(loss, 8, workspace, need))
+    return fail(TFD_EINVAL, "tfd_l2_loss_grad: overlapping buffers");
+  return hip_status(tfd::launch_l2_loss_grad(output, target, grad, loss, count, type == TFD_BF16, workspace,
+                                             as_stream(stream)),
+                    "tfd_l2_loss_grad launch");
+}
+
+tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delta, int64_t count,
+                                      uint16_t* var_bf16, void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_apply_gradient_descent: negative count");
+  if (count == 0) return TFD_OK;
+  if (!var || !delta) return fail(TFD_EINVAL, "tfd_apply_gradient_descent: NULL pointer");
+  const size_t bytes = (size_t)count * 4;
+  if (overlaps(var, bytes, delta, bytes) || overlaps(var_bf16, (size_t)count * 2, var, bytes) ||
+      overlaps(var_bf16, (size_t)count * 2, delta, bytes))
+    return fail(TFD_EINVAL, "tfd_apply_gradient_descent: overlapping buffers");
+  return hip_status(tfd::launch_sgd(var, alpha, delta, count, var_bf16, as_stream(stream)),
+                    "tfd_apply_gradient_descent launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,49 @@
+// Internal launch interface between the C ABI (api.cpp) and the kernels.
+// Callers have validated every argument; launchers only pick a kernel
+// variant and enqueue it on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tfd {
+
+struct GemmDesc {
+  bool ta, tb;
+  int64_t m, n, k;
+  const void* a;
+  int64_t lda;
+  const void* b;
+  int64_t ldb;
+  void* c;
+  int64_t ldc;
+  bool in_bf16, out_bf16;
+  const float* bias;
+  int epi;  // 0 none, 1 bias, 2 bias + relu
+};
+
+bool gemm_vector_ok(const GemmDesc& d, int elem_bytes);
+hipError_t launch_gemm(const GemmDesc& d, hipStream_t s);
+
+hipError_t launch_bias_add(const void* value, const float* bias, void* out, int64_t rows, int64_t cols,
+                           bool bf16, hipStream_t s);
+hipError_t launch_relu(const void* x, void* y, int64_t count, bool bf16, hipStream_t s);
+hipError_t launch_relu_grad(const void* g, const void* f, void* out, int64_t count, bool bf16,
+                            hipStream_t s);
+
+// Column reduction with optional Relu mask (features) and optional masked
+// output (backprops). Partial sums go to `ws` (reduction_ws_bytes).
+size_t reduction_ws_bytes(int64_t rows, int64_t cols, bool bf16);
+hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* out, float* db,
+                                          int64_t rows, int64_t cols, bool bf16, void* ws,
+                                          hipStream_t s);
+
+size_t loss_ws_bytes(int64_t count, bool bf16);
+hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, double* loss,
+                               int64_t count, bool bf16, void* ws, hipStream_t s);
+
+hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow,
+                      hipStream_t s);
+
+}  // namespace tfd

@@ -1,0 +1,195 @@
+// BiasAddGrad (the bias gradient of the broadcast Add, section 4.1 of the
+// paper), optionally fused with ReluGrad: one pass over the upstream
+// gradient G (and the stored Relu output H) that writes the masked gradient
+// dY and reduces it over the batch rows.
+//
+// Pass 1 (grid: column groups x row chunks): each thread owns one 16-byte
+// column chunk (4 fp32 / 8 bf16 columns) and walks the rows of its chunk with
+// a stride of 4, so a wavefront reads 1 KiB of one row per access. The four
+// row phases of a block are combined through LDS in a fixed order and the
+// block writes one fp32 partial per column. Pass 2 sums the partials of each
+// column in row-chunk order. The grid depends only on (rows, cols, type), so
+// the bits of the result do not change from call to call.
+
+#include "common.h"
+#include "kernels.h"
+
+namespace tfd {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kColChunks = 64;               // column chunks per block
+constexpr int kRowPhases = kThreads / kColChunks;
+constexpr int kTargetBlocks = 2048;
+
+struct ReducePlan {
+  int64_t col_groups, row_chunks, rows_per_chunk;
+};
+
+ReducePlan plan(int64_t rows, int64_t cols, int V) {
+  ReducePlan p;
+  p.col_groups = (cols + kColChunks * V - 1) / (kColChunks * V);
+  if (p.col_groups < 1) p.col_groups = 1;
+  int64_t want = (kTargetBlocks + p.col_groups - 1) / p.col_groups;
+  int64_t max_chunks = (rows + 4 * kRowPhases - 1) / (4 * kRowPhases);  // >= 16 rows per chunk
+  if (max_chunks < 1) max_chunks = 1;
+  if (want > max_chunks) want = max_chunks;
+  if (want < 1) want = 1;
+  p.rows_per_chunk = (rows + want - 1) / want;
+  p.row_chunks = p.rows_per_chunk > 0 ? (rows + p.rows_per_chunk - 1) / p.rows_per_chunk : 1;
+  if (p.row_chunks < 1) p.row_chunks = 1;
+  return p;
+}
+
+template <typename T> struct Chunk16;
+template <> struct Chunk16<float> {
+  static constexpr int V = 4;
+  __device__ static void load(const float* p, float (&x)[4]) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = v[e];
+  }
+  __device__ static void store(float* p, const float (&x)[4]) {
+    *reinterpret_cast<f32x4*>(p) = f32x4{x[0], x[1], x[2], x[3]};
+  }
+};
+template <> struct Chunk16<bf16> {
+  static constexpr int V = 8;
+  __device__ static void load(const bf16* p, float (&x)[8]) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = bf16_bits_to_f32(v[e] & 0xFFFFu);
+      x[2 * e + 1] = bf16_bits_to_f32(v[e] >> 16);
+    }
+  }
+  __device__ static void store(bf16* p, const float (&x)[8]) {
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = (uint32_t)bf16_bits(x[2 * e]) | ((uint32_t)bf16_bits(x[2 * e + 1]) << 16);
+    *reinterpret_cast<u32x4*>(p) = v;
+  }
+};
+
+__device__ __forceinline__ float masked(float g, float f) {
+  return __builtin_bit_cast(float, f > 0.0f ? __builtin_bit_cast(uint32_t, g) : 0u);
+}
+
+template <typename T, bool MASK, bool WRITE, bool VEC>
+__global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* g, const T* f, T* out,
+                                                                  float* partial, int64_t rows,
+                                                                  int64_t cols, int64_t rows_per_chunk) {
+  constexpr int V = Chunk16<T>::V;
+  __shared__ float sh[kRowPhases][kColChunks * V];
+  const int cv = threadIdx.x % kColChunks;
+  const int phase = threadIdx.x / kColChunks;
+  const int64_t c0 = ((int64_t)blockIdx.x * kColChunks + cv) * V;
+  const int64_t chunk = blockIdx.y;
+  const int64_t r_begin = chunk * rows_per_chunk;
+  const int64_t r_end = min(rows, r_begin + rows_per_chunk);
+
+  float acc[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) acc[e] = 0.0f;
+
+  if (c0 < cols) {
+    const bool full = VEC && (c0 + V <= cols);
+    for (int64_t r = r_begin + phase; r < r_end; r += kRowPhases) {
+      const int64_t base = r * cols + c0;
+      float x[V];
+      if (full) {
+        Chunk16<T>::load(g + base, x);
+        if (MASK) {
+          float m[V];
+          Chunk16<T>::load(f + base, m);
+#pragma unroll
+          for (int e = 0; e < V; ++e) x[e] = masked(x[e], m[e]);
+        }
+        if (WRITE) Chunk16<T>::store(out + base, x);
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] += x[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          if (c0 + e < cols) {
+            float v = load_f32(g + base + e);
+            if (MASK) v = masked(v, load_f32(f + base + e));
+            if (WRITE) store_from_f32(out + base + e, v);
+            acc[e] += v;
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < V; ++e) sh[phase][cv * V + e] = acc[e];
+  __syncthreads();
+  for (int i = threadIdx.x; i < kColChunks * V; i += kThreads) {
+    const int64_t c = (int64_t)blockIdx.x * kColChunks * V + i;
+    if (c < cols) {
+      float s = sh[0][i];
+#pragma unroll
+      for (int ph = 1; ph < kRowPhases; ++ph) s += sh[ph][i];
+      partial[chunk * cols + c] = s;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void colsum_final_kernel(const float* partial, float* db,
+                                                                int64_t row_chunks, int64_t cols) {
+  const int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.0f;
+  for (int64_t k = 0; k < row_chunks; ++k) s += partial[k * cols + c];
+  db[c] = s;
+}
+
+template <typename T>
+hipError_t launch_t(const T* g, const T* f, T* out, float* db, int64_t rows, int64_t cols, float* ws,
+                    hipStream_t s) {
+  constexpr int V = Chunk16<T>::V;
+  const ReducePlan p = plan(rows, cols, V);
+  auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  const bool vec = (cols % V == 0) && al(g) && (!f || al(f)) && (!out || al(out));
+  dim3 grid((unsigned)p.col_groups, (unsigned)p.row_chunks);
+#define TFD_LAUNCH(M, W, VE)                                                                      \
+  hipLaunchKernelGGL((colsum_partial_kernel<T, M, W, VE>), grid, kThreads, 0, s, g, f, out, ws, rows, \
+                     cols, p.rows_per_chunk)
+  const bool mask = f != nullptr, write = out != nullptr;
+  if (vec) {
+    if (mask && write) TFD_LAUNCH(true, true, true);
+    else if (mask) TFD_LAUNCH(true, false, true);
+    else if (write) TFD_LAUNCH(false, true, true);
+    else TFD_LAUNCH(false, false, true);
+  } else {
+    if (mask && write) TFD_LAUNCH(true, true, false);
+    else if (mask) TFD_LAUNCH(true, false, false);
+    else if (write) TFD_LAUNCH(false, true, false);
+    else TFD_LAUNCH(false, false, false);
+  }
+#undef TFD_LAUNCH
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned g2 = (unsigned)((cols + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(colsum_final_kernel, g2, kThreads, 0, s, (const float*)ws, db, p.row_chunks, cols);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t reduction_ws_bytes(int64_t rows, int64_t cols, bool bf16_t) {
+  const ReducePlan p = plan(rows, cols, bf16_t ? 8 : 4);
+  return (size_t)(p.row_chunks * cols) * sizeof(float);
+}
+
+hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* out, float* db,
+                                          int64_t rows, int64_t cols, bool bf16_t, void* ws,
+                                          hipStream_t s) {
+  if (bf16_t)
+    return launch_t<bf16>((const bf16*)g, (const bf16*)f, (bf16*)out, db, rows, cols, (float*)ws, s);
+  return launch_t<float>((const float*)g, (const float*)f, (float*)out, db, rows, cols, (float*)ws, s);
+}
+
+}  // namespace tfd

@@ -1,0 +1,126 @@
+"""One training step of a stack of dense layers, as a fixed sequence of
+libtfdense calls on one HIP stream.
+
+The order is the one a dependency-respecting executor of the paper's graph
+would take (section 3.1 runs a node once its inputs are ready; section 2's
+control dependencies order a Variable's readers before its writer):
+
+  forward  l = 1..L : H_l = Relu(H_{l-1} W_l + b_l)   (identity on the output layer)
+  cost              : G = H_L - T, L = 1/2 |G|^2     (or a given upstream gradient)
+  backward l = L..1 : dY_l, db_l = ReluGrad + BiasAddGrad(G_l, H_l)
+                      G_{l-1} = dX_l = dY_l W_l^T          (reads the old W_l)
+                      dW_l = H_{l-1}^T dY_l
+                      W_l -= lr dW_l ; b_l -= lr db_l      (after both reads of W_l)
+
+Stream order is the only synchronisation; nothing waits on the host inside a
+step. All tensors stay resident in device memory between steps.
+"""
+
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import tfdense as T
+from .workloads import Workload
+
+
+def _to_device(a: np.ndarray, act: str, device) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+class DenseStep:
+    """Device state and launch sequence of one step of workload ``w``."""
+
+    def __init__(self, w: Workload, inputs: dict, device="cuda"):
+        self.w = w
+        self.device = torch.device(device)
+        self.act = torch.bfloat16 if w.act == "bf16" else torch.float32
+        dev = self.device
+        L, N = w.layers, w.batch
+        self.x = _to_device(inputs["x"], w.act, dev)
+        self.weights = [_to_device(a, w.act, dev) for a in inputs["weights"]]
+        self.masters = None if inputs["masters"] is None else [_to_device(a, "f32", dev) for a in inputs["masters"]]
+        self.biases = [_to_device(a, "f32", dev) for a in inputs["biases"]]
+        self.target = None if inputs["target"] is None else _to_device(inputs["target"], w.act, dev)
+        self.upstream = None if inputs["upstream"] is None else _to_device(inputs["upstream"], w.act, dev)
+
+        self.h = [self.x] + [torch.empty(N, w.dims[l + 1], dtype=self.act, device=dev) for l in range(L)]
+        self.g = self.upstream if self.upstream is not None else torch.empty(N, w.dims[-1], dtype=self.act, device=dev)
+        self.dy = [torch.empty(N, w.dims[l + 1], dtype=self.act, device=dev) if w.relus[l] else None
+                   for l in range(L)]
+        self.dx = [torch.empty(N, w.dims[l], dtype=self.act, device=dev) for l in range(L)]
+        self.dw = [torch.empty(w.dims[l], w.dims[l + 1], dtype=torch.float32, device=dev) for l in range(L)]
+        self.db = [torch.empty(w.dims[l + 1], dtype=torch.float32, device=dev) for l in range(L)]
+        self.loss = torch.zeros(1, dtype=torch.float64, device=dev)
+
+        need = [T.tfd_reduction_workspace_size(N, w.dims[l + 1], self.act) for l in range(L)]
+        need.append(T.tfd_loss_workspace_size(N * w.dims[-1], self.act))
+        self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
+
+        # pristine copies of the Variables, to restart from the same state
+        self._saved = [t.clone() for t in self.variables()]
+
+    def variables(self):
+        out = list(self.weights) + list(self.biases)
+        if self.masters is not None:
+            out += list(self.masters)
+        return out
+
+    def restore(self):
+        """Reset the Variables to their initial values (stream-ordered copies)."""
+        for t, s in zip(self.variables(), self._saved):
+            t.copy_(s)
+
+    def run(self, mark=None):
+        """Enqueue one step. ``mark(name)`` (optional) is called between
+        launches, e.g. to record timing events."""
+        w, L = self.w, self.w.layers
+        ws = self.workspace
+        for l in range(L):
+            if mark:
+                mark(f"fwd{l + 1}")
+            T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l],
+                         epilogue="bias_relu" if w.relus[l] else "bias")
+        if self.upstream is None:
+            if mark:
+                mark("loss")
+            T.tfd_l2_loss_grad(self.h[L], self.target, self.g, self.loss, workspace=ws)
+        grad = self.g
+        for l in reversed(range(L)):
+            if mark:
+                mark(f"relugrad{l + 1}")
+            if w.relus[l]:
+                T.tfd_relu_grad_bias_add_grad(grad, self.h[l + 1], self.dy[l], self.db[l], workspace=ws)
+                dyl = self.dy[l]
+            else:
+                T.tfd_bias_add_grad(grad, self.db[l], workspace=ws)
+                dyl = grad
+            if mark:
+                mark(f"dx{l + 1}")
+            T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True)
+            if mark:
+                mark(f"dw{l + 1}")
+            T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True)
+            if w.update:
+                if mark:
+                    mark(f"sgd{l + 1}")
+                if self.masters is not None:
+                    T.tfd_apply_gradient_descent(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l])
+                else:
+                    T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l])
+                T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l])
+            grad = self.dx[l]
+        if mark:
+            mark("end")
+
+    def dy_of(self, l: int) -> torch.Tensor:
+        """dY of layer l (0-based): the masked gradient, or the incoming
+        gradient itself on an identity layer."""
+        if self.w.relus[l]:
+            return self.dy[l]
+        return self.g if l == self.w.layers - 1 else self.dx[l + 1]

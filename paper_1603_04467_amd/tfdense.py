@@ -1,0 +1,208 @@
+"""Python binding of libtfdense (argument marshalling only).
+
+Each function carries the name of the C entry point it calls and takes torch
+tensors that already live on the GPU; it derives sizes, leading dimensions
+and element types, passes ``data_ptr()`` and the current HIP stream, and
+raises ``TfdError`` on a non-OK status. All arithmetic happens in the
+library's HIP kernels. torch is used for device memory and streams only.
+
+The library must be built (``python -m paper_1603_04467_amd.build``); there is
+no fallback when it is missing.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtfdense.so")
+
+TFD_OK, TFD_EINVAL, TFD_EUNSUPPORTED, TFD_EHIP = 0, 1, 2, 3
+TFD_F32, TFD_BF16 = 0, 1
+EPILOGUES = {"none": 0, "bias": 1, "bias_relu": 2}
+
+EXPORTS = (
+    "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
+    "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
+    "tfd_relu_grad_bias_add_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
+    "tfd_apply_gradient_descent",
+)
+
+
+class TfdError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libtfdense (torch is imported first so that the library binds to
+    the HIP runtime torch already uses)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_1603_04467_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, vp, i32, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    sig = {
+        "tfd_abi_version": ([], i32),
+        "tfd_status_string": ([i32], ctypes.c_char_p),
+        "tfd_last_error": ([], ctypes.c_char_p),
+        "tfd_matmul": ([i32, i32, i64, i64, i64, vp, i64, i32, vp, i64, i32, vp, i64, i32, vp, i32, vp], i32),
+        "tfd_bias_add": ([vp, vp, vp, i64, i64, i32, vp], i32),
+        "tfd_relu": ([vp, vp, i64, i32, vp], i32),
+        "tfd_relu_grad": ([vp, vp, vp, i64, i32, vp], i32),
+        "tfd_reduction_workspace_size": ([i64, i64, i32], sz),
+        "tfd_bias_add_grad": ([vp, vp, i64, i64, i32, vp, sz, vp], i32),
+        "tfd_relu_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
+        "tfd_loss_workspace_size": ([i64, i32], sz),
+        "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
+        "tfd_apply_gradient_descent": ([vp, ctypes.c_float, vp, i64, vp, vp], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != TFD_OK:
+        raise TfdError(status, load().tfd_last_error().decode())
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return TFD_F32
+    if t.dtype == torch.bfloat16:
+        return TFD_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _rowmajor(t: torch.Tensor, name: str) -> int:
+    """Leading dimension of a 2-D row-major tensor (unit column stride)."""
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    if t.stride(1) != 1 and t.size(1) > 1:
+        raise ValueError(f"{name} must have unit column stride")
+    return max(t.stride(0), t.size(1), 1)
+
+
+def _flat(t: torch.Tensor, name: str):
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.numel()
+
+
+def tfd_abi_version() -> int:
+    return load().tfd_abi_version()
+
+
+def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogue="none", stream=None):
+    """c = epilogue(op(a) @ op(b)) (see include/tfdense.h)."""
+    lda, ldb, ldc = _rowmajor(a, "a"), _rowmajor(b, "b"), _rowmajor(c, "c")
+    m = a.size(1) if transpose_a else a.size(0)
+    k = a.size(0) if transpose_a else a.size(1)
+    kb = b.size(1) if transpose_b else b.size(0)
+    n = b.size(0) if transpose_b else b.size(1)
+    if kb != k or tuple(c.shape) != (m, n):
+        raise ValueError(f"shape mismatch: op(a) {m}x{k}, op(b) {kb}x{n}, c {tuple(c.shape)}")
+    if bias is not None and (bias.dtype != torch.float32 or bias.numel() != n or not bias.is_contiguous()):
+        raise ValueError("bias must be a contiguous fp32 vector of length n")
+    _check(load().tfd_matmul(int(transpose_a), int(transpose_b), m, n, k,
+                             _ptr(a), lda, _dtype(a), _ptr(b), ldb, _dtype(b), _ptr(c), ldc, _dtype(c),
+                             _ptr(bias), EPILOGUES[epilogue], _stream(stream)))
+    return c
+
+
+def tfd_bias_add(value, bias, out, stream=None):
+    rows, cols = value.shape
+    _flat(value, "value"), _flat(out, "out")
+    _check(load().tfd_bias_add(_ptr(value), _ptr(bias), _ptr(out), rows, cols, _dtype(value), _stream(stream)))
+    return out
+
+
+def tfd_relu(features, activations, stream=None):
+    n = _flat(features, "features")
+    _check(load().tfd_relu(_ptr(features), _ptr(activations), n, _dtype(features), _stream(stream)))
+    return activations
+
+
+def tfd_relu_grad(gradients, features, backprops, stream=None):
+    n = _flat(gradients, "gradients")
+    _check(load().tfd_relu_grad(_ptr(gradients), _ptr(features), _ptr(backprops), n, _dtype(gradients),
+                                _stream(stream)))
+    return backprops
+
+
+def tfd_reduction_workspace_size(rows, cols, dtype) -> int:
+    return load().tfd_reduction_workspace_size(rows, cols, TFD_BF16 if dtype == torch.bfloat16 else TFD_F32)
+
+
+def tfd_loss_workspace_size(count, dtype) -> int:
+    return load().tfd_loss_workspace_size(count, TFD_BF16 if dtype == torch.bfloat16 else TFD_F32)
+
+
+def _workspace(nbytes, device, workspace):
+    if workspace is not None:
+        return workspace
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def tfd_relu_grad_bias_add_grad(gradients, features, backprops, bias_grad, workspace=None, stream=None):
+    rows, cols = gradients.shape
+    _flat(gradients, "gradients")
+    need = tfd_reduction_workspace_size(rows, cols, gradients.dtype)
+    ws = _workspace(need, gradients.device, workspace)
+    _check(load().tfd_relu_grad_bias_add_grad(_ptr(gradients), _ptr(features), _ptr(backprops), _ptr(bias_grad),
+                                              rows, cols, _dtype(gradients), _ptr(ws), ws.numel(),
+                                              _stream(stream)))
+    return backprops, bias_grad
+
+
+def tfd_bias_add_grad(out_backprop, bias_grad, workspace=None, stream=None):
+    rows, cols = out_backprop.shape
+    _flat(out_backprop, "out_backprop")
+    need = tfd_reduction_workspace_size(rows, cols, out_backprop.dtype)
+    ws = _workspace(need, out_backprop.device, workspace)
+    _check(load().tfd_bias_add_grad(_ptr(out_backprop), _ptr(bias_grad), rows, cols, _dtype(out_backprop),
+                                    _ptr(ws), ws.numel(), _stream(stream)))
+    return bias_grad
+
+
+def tfd_l2_loss_grad(output, target, grad, loss, workspace=None, stream=None):
+    n = _flat(output, "output")
+    need = tfd_loss_workspace_size(n, output.dtype)
+    ws = _workspace(need, output.device, workspace)
+    _check(load().tfd_l2_loss_grad(_ptr(output), _ptr(target), _ptr(grad), _ptr(loss), n, _dtype(output),
+                                   _ptr(ws), ws.numel(), _stream(stream)))
+    return grad, loss
+
+
+def tfd_apply_gradient_descent(var, alpha, delta, var_bf16=None, stream=None):
+    n = _flat(var, "var")
+    if var.dtype != torch.float32 or delta.dtype != torch.float32:
+        raise TypeError("Variables and their deltas are fp32")
+    if var_bf16 is not None and var_bf16.dtype != torch.bfloat16:
+        raise TypeError("the 16-bit copy must be bfloat16")
+    _check(load().tfd_apply_gradient_descent(_ptr(var), float(alpha), _ptr(delta), n, _ptr(var_bf16),
+                                             _stream(stream)))
+    return var

@@ -1,0 +1,101 @@
+"""The C-ABI library loads, exports every entry point that include/tfdense.h
+declares, and rejects invalid arguments before launching anything (these
+checks run without a GPU: no call here reaches a kernel launch)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tfdense.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"TFD_API\s+[\w\s\*]+?\b(tfd_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_1603_04467_amd import build, tfdense
+    if not os.path.exists(tfdense.LIB_PATH):
+        build.build()
+    return tfdense.load()
+
+
+def test_header_declares_the_op_set():
+    names = _declared()
+    for op in ("tfd_matmul", "tfd_bias_add", "tfd_relu", "tfd_relu_grad", "tfd_bias_add_grad",
+               "tfd_relu_grad_bias_add_grad", "tfd_l2_loss_grad", "tfd_apply_gradient_descent"):
+        assert op in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_1603_04467_amd import tfdense
+    names = _declared()
+    assert set(names) == set(tfdense.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings(lib):
+    assert lib.tfd_abi_version() == 1
+    assert lib.tfd_status_string(0) == b"ok"
+    assert lib.tfd_status_string(1) == b"invalid argument"
+    assert lib.tfd_status_string(2) == b"unsupported"
+    assert lib.tfd_status_string(3) == b"HIP runtime error"
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def test_matmul_validation(lib):
+    mm = lib.tfd_matmul
+    # negative size
+    assert mm(0, 0, -1, 2, 3, FAKE, 3, 0, FAKE, 2, 0, FAKE * 4, 2, 0, None, 0, None) == 1
+    assert b"negative" in lib.tfd_last_error()
+    # leading dimension too small (A is m x k = 4 x 8, lda 7)
+    assert mm(0, 0, 4, 4, 8, FAKE, 7, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 0, None) == 1
+    assert b"leading dimension" in lib.tfd_last_error()
+    # NULL output
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, None, 4, 0, None, 0, None) == 1
+    # bias epilogue without a bias
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 2, None) == 1
+    # unsupported type combinations and both transposes
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 1, FAKE * 4, 4, 0, None, 0, None) == 2
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 1, None, 0, None) == 2
+    assert mm(1, 1, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 0, None) == 2
+    # unknown dtype / epilogue
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 7, FAKE * 2, 4, 7, FAKE * 4, 4, 7, None, 0, None) == 1
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 9, None) == 1
+    # output overlapping an input
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE + 16, 4, 0, None, 0, None) == 1
+    assert b"overlap" in lib.tfd_last_error()
+    # empty output: a successful no-op, even with NULL pointers
+    assert mm(0, 0, 0, 4, 4, None, 4, 0, None, 4, 0, None, 4, 0, None, 0, None) == 0
+    assert mm(0, 0, 4, 0, 4, None, 4, 0, None, 1, 0, None, 1, 0, None, 0, None) == 0
+
+
+def test_elementwise_and_reduction_validation(lib):
+    assert lib.tfd_relu(None, None, -1, 0, None) == 1
+    assert lib.tfd_relu(None, None, 0, 0, None) == 0
+    assert lib.tfd_relu(None, FAKE, 5, 0, None) == 1
+    assert lib.tfd_relu(FAKE, FAKE + 4, 5, 0, None) == 1          # partial overlap
+    assert lib.tfd_relu_grad(FAKE, FAKE * 2, FAKE * 2, 5, 0, None) == 1  # backprops aliases features
+    assert lib.tfd_bias_add(FAKE, FAKE * 2, FAKE * 3, -1, 3, 0, None) == 1
+    need = lib.tfd_reduction_workspace_size(1000, 300, 0)
+    assert need > 0
+    assert lib.tfd_reduction_workspace_size(1000, 300, 0) == need  # depends only on the shape
+    # workspace too small
+    st = lib.tfd_relu_grad_bias_add_grad(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 1000, 300, 0, FAKE * 5,
+                                         need - 1, None)
+    assert st == 1 and b"workspace" in lib.tfd_last_error()
+    st = lib.tfd_bias_add_grad(FAKE, FAKE * 4, 1000, 300, 0, None, 0, None)
+    assert st == 1 and lib.tfd_last_error().startswith(b"tfd_bias_add_grad")
+    lneed = lib.tfd_loss_workspace_size(1000, 0)
+    assert lneed >= 8
+    assert lib.tfd_l2_loss_grad(FAKE, None, FAKE * 2, None, 1000, 0, FAKE * 3, lneed, None) == 1
+    assert lib.tfd_apply_gradient_descent(FAKE, ctypes.c_float(0.01), FAKE + 8, 100, None, None) == 1
+    assert lib.tfd_apply_gradient_descent(None, ctypes.c_float(0.01), None, 0, None, None) == 0

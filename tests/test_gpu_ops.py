@@ -1,0 +1,289 @@
+"""Per-op parity of the HIP kernels against the oracle, through the C ABI.
+
+Inputs are seeded host arrays handed to both sides; the oracle never sees a
+value produced on the GPU. Shapes span several tiles of every GEMM tile
+configuration, ragged tails, unaligned rows (the per-element load path) and
+strided leading dimensions.
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1603_04467_amd import tfdense as T
+from paper_1603_04467_amd.workloads import to_bf16_bits
+from tests.parity import TAU, amax, assert_bits, assert_close, mask_mismatch, to_f64
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _host(rng, shape, dt, scale=1.0, kind="normal"):
+    """Seeded operand: float64 values exactly representable in `dt` and the
+    matching device tensor."""
+    if kind == "normal":
+        a = (rng.standard_normal(shape) * scale).astype(np.float32)
+    elif kind == "int":
+        a = rng.integers(-2, 3, size=shape).astype(np.float32)
+    else:
+        raise ValueError(kind)
+    if dt == "bf16":
+        bits = to_bf16_bits(a)
+        t = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+        return oracle.bf16_bits_to_f64(bits), t
+    return a.astype(np.float64), torch.from_numpy(a).to(DEV)
+
+
+def _empty(shape, dt, ld=None):
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    if ld is None or ld == shape[1]:
+        return torch.full(shape, float("nan"), dtype=tdt, device=DEV)
+    big = torch.full((shape[0], ld), float("nan"), dtype=tdt, device=DEV)
+    return big[:, : shape[1]]
+
+
+def _strided(host, t, extra):
+    """Copy `t` into a wider buffer so that its leading dimension grows by `extra`."""
+    if extra == 0:
+        return t
+    big = torch.zeros(t.shape[0], t.shape[1] + extra, dtype=t.dtype, device=DEV)
+    big[:, : t.shape[1]] = t
+    return big[:, : t.shape[1]]
+
+
+def _run_gemm(m, n, k, layout, din, dout, epi, seed=0, kind="normal", ld_extra=0, tile=None):
+    rng = np.random.default_rng([seed, m, n, k])
+    ta, tb = layout == "TN", layout == "NT"
+    a_h, a = _host(rng, (k, m) if ta else (m, k), din, kind=kind)
+    b_h, b = _host(rng, (n, k) if tb else (k, n), din, kind=kind)
+    a, b = _strided(a_h, a, ld_extra), _strided(b_h, b, ld_extra)
+    bias_h = bias = None
+    if epi != "none":
+        bias_h = (rng.standard_normal(n) * 0.5).astype(np.float32)
+        bias = torch.from_numpy(bias_h).to(DEV)
+        bias_h = bias_h.astype(np.float64)
+    c = _empty((m, n), dout, ld=n + ld_extra if ld_extra else None)
+    old = os.environ.get("TFD_GEMM_TILE")
+    if tile is not None:
+        os.environ["TFD_GEMM_TILE"] = str(tile)
+    try:
+        T.tfd_matmul(a, b, c, transpose_a=ta, transpose_b=tb, bias=bias, epilogue=epi)
+        torch.cuda.synchronize()
+    finally:
+        if tile is not None:
+            if old is None:
+                del os.environ["TFD_GEMM_TILE"]
+            else:
+                os.environ["TFD_GEMM_TILE"] = old
+    want = oracle.matmul(a_h, b_h, ta, tb, out=dout, bias=bias_h, relu=epi == "bias_relu")
+    pre = oracle.matmul(a_h, b_h, ta, tb, out="f64", bias=bias_h)
+    D = k * amax(a_h) * amax(b_h) + (amax(bias_h) if bias_h is not None else 0.0)
+    return to_f64(c), want, pre, D
+
+
+SHAPES = [(1, 1, 1), (3, 5, 7), (32, 32, 32), (64, 64, 64), (65, 33, 17), (100, 100, 784),
+          (127, 129, 200), (256, 10, 1024), (300, 264, 136), (513, 256, 96), (1000, 784, 100)]
+TYPES = [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")]
+
+
+@pytest.mark.parametrize("din,dout", TYPES)
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("m,n,k", SHAPES)
+def test_matmul_parity(m, n, k, layout, din, dout):
+    epi = "bias_relu" if layout == "NN" else "none"
+    got, want, pre, D = _run_gemm(m, n, k, layout, din, dout, epi)
+    assert_close(got, want, D, TAU[din], f"{layout} {din}->{dout} {m}x{n}x{k}")
+    if epi == "bias_relu":
+        assert not np.any(np.signbit(got)), "Relu output with a sign bit"
+        bad, _ = mask_mismatch(got, pre, TAU[din] * D)
+        assert bad == 0, f"{bad} Relu mask decisions differ outside the rounding band"
+
+
+@pytest.mark.parametrize("tile", [1, 2, 3, 4])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("din,dout", TYPES)
+def test_matmul_every_tile_config(tile, layout, din, dout):
+    m, n, k = 600, 520, 264   # ragged against 256 and 128 in m, several k-tiles
+    got, want, pre, D = _run_gemm(m, n, k, layout, din, dout, "bias", seed=tile, tile=tile)
+    assert_close(got, want, D, TAU[din], f"tile {tile} {layout} {din}->{dout}")
+
+
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("din", ["f32", "bf16"])
+def test_matmul_small_integers_exact(layout, din):
+    # integer operands in [-2, 2]: every partial sum is an exact integer < 2**24,
+    # |C| <= 4 * 64 = 256 is exact in both output types
+    got, want, _, _ = _run_gemm(200, 136, 64, layout, din, din, "none", kind="int")
+    assert_bits(got, want, f"integer {layout} {din}")
+
+
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_matmul_identity_and_permutation_bit_exact(layout, dt):
+    rng = np.random.default_rng(9)
+    n = 136
+    x_h, x = _host(rng, (264, n), dt)
+    perm = rng.permutation(n)
+    P = np.eye(n)[:, perm]
+    P_dev = torch.from_numpy(P.astype(np.float32)).to(DEV).to(x.dtype)
+    out = _empty((264, n), dt)
+    if layout == "NN":
+        T.tfd_matmul(x, P_dev, out)                                   # x @ P
+        want = x_h[:, perm]
+    elif layout == "NT":
+        T.tfd_matmul(x, P_dev.t().contiguous(), out, transpose_b=True)  # x @ (P^T)^T
+        want = x_h[:, perm]
+    else:
+        xt = x.t().contiguous()
+        T.tfd_matmul(xt, P_dev, out, transpose_a=True)               # (x^T)^T @ P
+        want = x_h[:, perm]
+    torch.cuda.synchronize()
+    assert_bits(to_f64(out), want, f"permutation {layout} {dt}")
+
+
+@pytest.mark.parametrize("ld_extra", [4, 8, 24])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_matmul_leading_dimensions(layout, ld_extra):
+    got, want, _, D = _run_gemm(130, 72, 88, layout, "f32", "f32", "bias", ld_extra=ld_extra)
+    assert_close(got, want, D, TAU["f32"], f"ld+{ld_extra} {layout}")
+    got, want, _, D = _run_gemm(130, 72, 88, layout, "bf16", "bf16", "bias", ld_extra=ld_extra)
+    assert_close(got, want, D, TAU["bf16"], f"ld+{ld_extra} {layout} bf16")
+
+
+def test_matmul_k_zero_gives_relu_of_bias():
+    bias = torch.tensor([0.5, -1.0, 0.0, 2.0], device=DEV)
+    a = torch.empty(3, 0, device=DEV)
+    b = torch.empty(0, 4, device=DEV)
+    c = torch.full((3, 4), float("nan"), device=DEV)
+    T.tfd_matmul(a, b, c, bias=bias, epilogue="bias_relu")
+    torch.cuda.synchronize()
+    assert_bits(to_f64(c), np.array([[0.5, 0.0, 0.0, 2.0]] * 3), "k=0")
+
+
+def test_matmul_is_deterministic():
+    a = torch.randn(1000, 777, device=DEV)
+    b = torch.randn(777, 512, device=DEV)
+    c1 = torch.empty(1000, 512, device=DEV)
+    c2 = torch.empty(1000, 512, device=DEV)
+    T.tfd_matmul(a, b, c1)
+    T.tfd_matmul(a, b, c2)
+    torch.cuda.synchronize()
+    assert torch.equal(c1, c2)
+
+
+# ---------------------------------------------------------------- element-wise
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("count", [1, 7, 8, 1000, 4096 * 3 + 5])
+def test_relu_and_relu_grad_bit_exact(dt, count):
+    rng = np.random.default_rng(count)
+    x_h, x = _host(rng, (count,), dt)
+    x[: min(count, 3)] = torch.tensor([0.0, -0.0, -1.0], dtype=x.dtype, device=DEV)[: min(count, 3)]
+    x_h = to_f64(x)
+    g_h, g = _host(rng, (count,), dt)
+    y = torch.empty_like(x)
+    T.tfd_relu(x, y)
+    bp = torch.empty_like(x)
+    T.tfd_relu_grad(g, x, bp)
+    torch.cuda.synchronize()
+    assert_bits(to_f64(y), oracle.relu(x_h), "relu")
+    assert_bits(to_f64(bp), oracle.relu_grad(g_h, x_h), "relu_grad")
+    # in place
+    T.tfd_relu(x, x)
+    torch.cuda.synchronize()
+    assert_bits(to_f64(x), oracle.relu(x_h), "relu in place")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,cols", [(1, 1), (5, 10), (64, 4096), (33, 1029)])
+def test_bias_add(dt, rows, cols):
+    rng = np.random.default_rng(rows * 7 + cols)
+    v_h, v = _host(rng, (rows, cols), dt)
+    b32 = rng.standard_normal(cols).astype(np.float32)
+    out = torch.empty_like(v)
+    T.tfd_bias_add(v, torch.from_numpy(b32).to(DEV), out)
+    torch.cuda.synchronize()
+    want = oracle.bias_add(v_h, b32.astype(np.float64), out=dt)
+    if dt == "f32":
+        assert_bits(to_f64(out), want, "bias_add f32")   # one correctly rounded fp32 add
+    else:
+        assert_close(to_f64(out), want, amax(v_h) + float(np.max(np.abs(b32))), TAU["bf16"], "bias_add bf16")
+
+
+@pytest.mark.parametrize("count", [1, 3, 4, 1000, 16 * 1024 + 3])
+@pytest.mark.parametrize("shadow", [False, True])
+def test_apply_gradient_descent_bit_exact(count, shadow):
+    rng = np.random.default_rng(count)
+    var = rng.standard_normal(count).astype(np.float32)
+    delta = (rng.standard_normal(count) * 10.0 ** rng.integers(-6, 4, count)).astype(np.float32)
+    v = torch.from_numpy(var).to(DEV)
+    d = torch.from_numpy(delta).to(DEV)
+    sh = torch.empty(count, dtype=torch.bfloat16, device=DEV) if shadow else None
+    T.tfd_apply_gradient_descent(v, 0.01, d, var_bf16=sh)
+    torch.cuda.synchronize()
+    want = oracle.apply_gradient_descent(var, np.float32(0.01), delta)
+    assert_bits(to_f64(v), want, "sgd")
+    if shadow:
+        assert_bits(to_f64(sh), oracle.round_bf16(want), "sgd shadow")
+
+
+def test_apply_gradient_descent_lr_zero_is_identity():
+    var = torch.randn(12345, device=DEV)
+    keep = var.clone()
+    T.tfd_apply_gradient_descent(var, 0.0, torch.randn(12345, device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(var, keep)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("count", [1, 9, 100 * 100, 256 * 10, 1 << 20])
+@pytest.mark.parametrize("with_target", [False, True])
+def test_l2_loss_grad(dt, count, with_target):
+    rng = np.random.default_rng(count + with_target)
+    o_h, o = _host(rng, (count,), dt)
+    t_h, t = _host(rng, (count,), dt) if with_target else (None, None)
+    g = torch.empty_like(o)
+    loss = torch.zeros(1, dtype=torch.float64, device=DEV)
+    T.tfd_l2_loss_grad(o, t, g, loss)
+    torch.cuda.synchronize()
+    g_want, l_want = oracle.l2_loss_grad(o_h, t_h, grad_dtype=dt)
+    assert_bits(to_f64(g), g_want, "loss gradient")
+    assert abs(loss.item() - l_want) <= 1e-6 * l_want
+
+
+# ---------------------------------------------------------------- reductions
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("rows,cols", [(1, 1), (3, 5), (16, 4096), (1000, 300), (257, 1029), (8192, 4096),
+                                       (0, 7)])
+@pytest.mark.parametrize("mask", [True, False])
+def test_relu_grad_bias_add_grad(dt, rows, cols, mask):
+    rng = np.random.default_rng([rows, cols, mask])
+    g_h, g = _host(rng, (rows, cols), dt)
+    f_h, f = _host(rng, (rows, cols), dt)
+    db = torch.full((cols,), float("nan"), device=DEV)
+    if mask:
+        bp = torch.empty_like(g)
+        T.tfd_relu_grad_bias_add_grad(g, f, bp, db)
+        dy = oracle.relu_grad(g_h, f_h)
+    else:
+        T.tfd_bias_add_grad(g, db)
+        dy = g_h
+    torch.cuda.synchronize()
+    if mask:
+        assert_bits(to_f64(bp), dy, "ReluGrad output")
+    want = oracle.bias_add_grad(dy)
+    D = max(rows, 1) * max(amax(dy), 1e-30)
+    assert_close(to_f64(db), want, D, TAU["f32"], "BiasAddGrad")
+    # the summation order is fixed: a second call gives the same bits
+    db2 = torch.empty_like(db)
+    if mask:
+        T.tfd_relu_grad_bias_add_grad(g, f, None, db2)
+    else:
+        T.tfd_bias_add_grad(g, db2)
+    torch.cuda.synchronize()
+    assert torch.equal(db, db2)

@@ -1,0 +1,282 @@
+"""End-to-end parity of one training step (the exact launch sequence that
+bench.py times) against the oracle's chain from the same seeded inputs.
+
+Forward tensors, the loss and the output layer's gradients are continuous in
+the rounding errors and are compared with the normalised-error rule. Below a
+Relu, a mask decision on a pre-activation inside the rounding band of zero
+may legitimately differ between the GPU and the oracle (both are correct
+steps of the method); such a flip changes the whole row of every input
+gradient below it. The checks therefore
+  - require every mask difference to lie inside the band (and count them),
+  - compare row-local tensors (dY, dX) on the rows no flip touched,
+  - bound the batch reductions (dW, db) by tau * D plus the largest change
+    the touched rows can make,
+  - check on the GPU's own tensors that dY is exactly G where H > 0 and +0
+    elsewhere, and the per-layer adjoint identity
+    <G_l, H_l> = <W_l, dW_l> + <b_l, db_l>.
+At the full sizes the oracle runs the whole forward pass and the output
+layer's backward pass, and the Relu layers' input gradients on sampled rows.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1603_04467_amd import workloads
+from paper_1603_04467_amd.step import DenseStep
+from tests.parity import TAU, amax, assert_bits, assert_close, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_inputs(w, inp):
+    conv = oracle.bf16_bits_to_f64 if w.act == "bf16" else (lambda a: a.astype(np.float64))
+    return {
+        "x": conv(inp["x"]),
+        "weights": [conv(a) for a in inp["weights"]],
+        "masters": None if inp["masters"] is None else [a.astype(np.float64) for a in inp["masters"]],
+        "biases": [a.astype(np.float64) for a in inp["biases"]],
+        "target": None if inp["target"] is None else conv(inp["target"]),
+        "upstream": None if inp["upstream"] is None else conv(inp["upstream"]),
+    }
+
+
+def _assert_within(got, want, allowed, what):
+    got = np.asarray(got, np.float64)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite"
+    if got.size == 0:
+        return
+    e = float(np.max(np.abs(got - want)))
+    assert e <= allowed, f"{what}: max|err| = {e:.3e} > allowed {allowed:.3e}"
+
+
+def _run_gpu(w, inp):
+    s = DenseStep(w, inp)
+    s.run()
+    torch.cuda.synchronize()
+    return s
+
+
+def _flip_rows(h_gpu, y_ref, band, what):
+    """Rows where the GPU's Relu decision differs from the sign of the
+    oracle's pre-activation; every such element must be inside the band."""
+    diff = (h_gpu > 0) != (y_ref > 0)
+    outside = diff & (np.abs(y_ref) > band)
+    assert not np.any(outside), f"{what}: {int(outside.sum())} mask decisions differ outside the band"
+    return np.any(diff, axis=1)
+
+
+def _check_mask_consistency(s, l):
+    """dY = G where the stored H > 0, +0 elsewhere (bit for bit, GPU tensors)."""
+    g = s.g if l == s.w.layers - 1 else s.dx[l + 1]
+    h = s.h[l + 1]
+    want = torch.where(h > 0, g, torch.zeros_like(g))
+    assert torch.equal(s.dy[l], want), f"layer {l + 1}: dY is not G masked by H > 0"
+    assert not torch.any(torch.signbit(h)), f"layer {l + 1}: Relu output with a sign bit"
+
+
+def _check_adjoint(s, l, tau):
+    """<G_l, H_l> = <W_l, dW_l> + <b_l, db_l> on the GPU's tensors."""
+    g = to_f64(s.g if l == s.w.layers - 1 else s.dx[l + 1])
+    h = to_f64(s.h[l + 1])
+    x = to_f64(s.h[l])
+    dy = to_f64(s.dy_of(l))
+    W = s._saved[l].float().cpu().numpy().astype(np.float64)
+    b = s._saved[len(s.weights) + l].cpu().numpy().astype(np.float64)
+    dw = to_f64(s.dw[l])
+    db = to_f64(s.db[l])
+    lhs = float(np.sum(g * h))
+    rhs = float(np.sum(W * dw) + np.sum(b * db))
+    K = x.shape[1]
+    D = float(np.sum(np.abs(dy))) * (K * amax(x) * amax(W) + amax(b))
+    assert abs(lhs - rhs) <= tau * D, f"layer {l + 1}: adjoint identity off by {abs(lhs - rhs):.3e} (D {D:.3e})"
+
+
+def _compare_full(w, inp, s):
+    """Whole-step comparison against the oracle's full chain."""
+    hi = _host_inputs(w, inp)
+    tau = TAU[w.act]
+    L = w.layers
+    ref = oracle.dense_step(hi["x"], hi["weights"], hi["biases"], list(w.relus), act=w.act,
+                            target=hi["target"], upstream_grad=hi["upstream"], lr=w.lr,
+                            masters=hi["masters"], update=w.update)
+    h_gpu = [to_f64(t) for t in s.h]
+    # forward
+    D_fwd = []
+    for l in range(L):
+        D = w.dims[l] * amax(ref["h"][l]) * amax(hi["weights"][l]) + amax(hi["biases"][l])
+        D_fwd.append(D)
+        assert_close(h_gpu[l + 1], ref["h"][l + 1], D, tau, f"H_{l + 1}")
+    # mask flips (rows touched, cumulated from the top)
+    touched = np.zeros(w.batch, dtype=bool)
+    touched_at = [None] * L
+    flips = 0
+    for l in reversed(range(L)):
+        if w.relus[l]:
+            y = oracle.matmul(ref["h"][l], hi["weights"][l], out="f64", bias=hi["biases"][l])
+            rows = _flip_rows(h_gpu[l + 1], y, tau * D_fwd[l], f"layer {l + 1}")
+            flips += int(rows.sum())
+            touched |= rows
+        touched_at[l] = touched.copy()
+    # cost
+    g_gpu = to_f64(s.g)
+    if ref["loss"] is not None:
+        D_G = D_fwd[-1] + amax(ref["g"])
+        assert_close(g_gpu, ref["g"], D_G, tau, "G")
+        allowed = tau * D_fwd[-1] * float(np.sum(np.abs(ref["g"]))) + 1e-12 * ref["loss"]
+        _assert_within(np.array([s.loss.item()]), np.array([ref["loss"]]), allowed, "loss")
+    else:
+        D_G = amax(ref["g"])
+        assert_bits(g_gpu, ref["g"], "upstream gradient")
+    # backward
+    D_g = D_G
+    for l in reversed(range(L)):
+        keep = ~touched_at[l]
+        nt = int((~keep).sum())
+        dy_ref = ref["dy"][l]
+        dy_gpu = to_f64(s.dy_of(l))
+        if w.relus[l]:
+            _check_mask_consistency(s, l)
+            assert_close(dy_gpu[keep], dy_ref[keep], D_g, tau, f"dY_{l + 1}")
+        W = hi["weights"][l]
+        M = w.dims[l + 1]
+        md = amax(dy_ref)
+        D_dx = M * md * amax(W)
+        assert_close(to_f64(s.dx[l])[keep], ref["dx"][l][keep], D_dx, tau, f"dX_{l + 1}")
+        mh = amax(ref["h"][l])
+        _assert_within(to_f64(s.dw[l]), ref["dw"][l], tau * w.batch * mh * md + 2 * nt * mh * md, f"dW_{l + 1}")
+        _assert_within(to_f64(s.db[l]), ref["db"][l], tau * w.batch * md + 2 * nt * md, f"db_{l + 1}")
+        _check_adjoint(s, l, tau)
+        if w.update:
+            allowed_w = w.lr * (tau * w.batch * mh * md + 2 * nt * mh * md)
+            if s.masters is not None:
+                mw = amax(ref["new_masters"][l])
+                _assert_within(to_f64(s.masters[l]), ref["new_masters"][l], allowed_w + 2.0 ** -23 * mw, f"W_{l + 1}")
+                _assert_within(to_f64(s.weights[l]), ref["new_weights"][l], allowed_w + 2.0 ** -8 * mw, f"W16_{l + 1}")
+            else:
+                mw = amax(ref["new_weights"][l])
+                _assert_within(to_f64(s.weights[l]), ref["new_weights"][l], allowed_w + 2.0 ** -23 * mw, f"W_{l + 1}")
+            allowed_b = w.lr * (tau * w.batch * md + 2 * nt * md) + 2.0 ** -23 * amax(ref["new_biases"][l])
+            _assert_within(to_f64(s.biases[l]), ref["new_biases"][l], allowed_b, f"b_{l + 1}")
+        else:
+            assert torch.equal(s.weights[l], s._saved[l])
+        D_g = D_dx
+    return flips
+
+
+SCALED = [
+    ("dense784x100", None, None),
+    ("mlp784-1024-1024-10", None, None),
+    ("wide4096x4-f32", 600, (256, 384, 264, 128, 200)),
+    ("wide4096x4-f32", 520, (136, 256, 512, 264, 128)),
+    ("wide4096x4-bf16", 600, (256, 384, 264, 128, 200)),
+    ("wide4096x4-bf16", 1032, (512, 768, 512, 256, 512)),
+    ("tall512x32768-bf16", 1000, (512, 2048)),
+    ("tall512x32768-bf16", 264, (96, 4104)),
+    ("tall512x32768-bf16", 130, (100, 1030)),
+]
+
+
+@pytest.mark.parametrize("name,batch,dims", SCALED)
+def test_step_matches_oracle(name, batch, dims):
+    w = workloads.workload(name)
+    if batch is not None:
+        w = w.scaled(batch=batch, dims=dims)
+    inp = workloads.generate(w, seed=0)
+    s = _run_gpu(w, inp)
+    flips = _compare_full(w, inp, s)
+    print(f"{w.name}: {flips} rows with in-band Relu mask differences")
+
+
+@pytest.mark.parametrize("name", ["dense784x100", "wide4096x4-bf16"])
+def test_step_is_deterministic(name):
+    w = workloads.workload(name)
+    if name != "dense784x100":
+        w = w.scaled(batch=1032, dims=(512, 768, 512, 256, 512))
+    inp = workloads.generate(w, seed=3)
+    s = DenseStep(w, inp)
+    s.run()
+    first = [t.clone() for t in s.dx + s.dw + s.db + s.variables()] + [s.loss.clone()]
+    s.restore()
+    s.run()
+    torch.cuda.synchronize()
+    second = [t for t in s.dx + s.dw + s.db + s.variables()] + [s.loss]
+    for a, b in zip(first, second):
+        assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- full sizes
+
+def _sampled_rows(n, count=48, seed=0):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([[0, n - 1], rng.choice(n, size=min(count, n), replace=False)]))
+
+
+def _check_full_size(name):
+    """Full-size step: the oracle's whole forward pass, the output layer's
+    backward pass in full, the Relu layers' input gradients on sampled rows,
+    and the identities on the GPU's own tensors."""
+    w = workloads.workload(name)
+    inp = workloads.generate(w, seed=0)
+    s = _run_gpu(w, inp)
+    hi = _host_inputs(w, inp)
+    tau = TAU[w.act]
+    L = w.layers
+    if L == 1:
+        return _compare_full(w, inp, s)
+    # forward in full (continuous: compared everywhere)
+    h_ref = [hi["x"]]
+    D_fwd = []
+    y_ref = []
+    for l in range(L):
+        D = w.dims[l] * amax(h_ref[l]) * amax(hi["weights"][l]) + amax(hi["biases"][l])
+        y = oracle.matmul(h_ref[l], hi["weights"][l], out="f64", bias=hi["biases"][l])
+        h = oracle.round_to(oracle.relu(y) if w.relus[l] else y, w.act)
+        y_ref.append(y)
+        h_ref.append(h)
+        D_fwd.append(D)
+        assert_close(to_f64(s.h[l + 1]), h, D, tau, f"H_{l + 1}")
+    g_ref, loss_ref = oracle.l2_loss_grad(h_ref[L], hi["target"], grad_dtype=w.act)
+    D_G = D_fwd[-1] + amax(g_ref)
+    assert_close(to_f64(s.g), g_ref, D_G, tau, "G")
+    allowed = tau * D_fwd[-1] * float(np.sum(np.abs(g_ref))) + 1e-12 * loss_ref
+    _assert_within(np.array([s.loss.item()]), np.array([loss_ref]), allowed, "loss")
+    # mask decisions of every Relu layer: in-band only
+    touched = np.zeros(w.batch, dtype=bool)
+    for l in range(L):
+        if w.relus[l]:
+            touched |= _flip_rows(to_f64(s.h[l + 1]), y_ref[l], tau * D_fwd[l], f"layer {l + 1}")
+    # output (identity) layer: no mask above it, compared in full
+    top = L - 1
+    assert not w.relus[top]
+    md = amax(g_ref)
+    mh = amax(h_ref[top])
+    dx_top = oracle.matmul(g_ref, hi["weights"][top], transpose_b=True, out=w.act)
+    assert_close(to_f64(s.dx[top]), dx_top, w.dims[-1] * md * amax(hi["weights"][top]), tau, f"dX_{L}")
+    assert_close(to_f64(s.dw[top]), oracle.matmul(h_ref[top], g_ref, transpose_a=True, out="f32"),
+                 w.batch * mh * md, tau, f"dW_{L}")
+    assert_close(to_f64(s.db[top]), oracle.bias_add_grad(g_ref), w.batch * md, tau, f"db_{L}")
+    # Relu layers: row-local chain on sampled rows the flips did not touch
+    rows = _sampled_rows(w.batch)
+    rows = rows[~touched[rows]]
+    g_rows = dx_top[rows]
+    D_g = w.dims[-1] * md * amax(hi["weights"][top])
+    for l in reversed(range(top)):
+        dy_rows = oracle.relu_grad(g_rows, h_ref[l + 1][rows])
+        assert_close(to_f64(s.dy[l])[rows], dy_rows, D_g, tau, f"dY_{l + 1} (sampled rows)")
+        dx_rows = oracle.matmul(dy_rows, hi["weights"][l], transpose_b=True, out=w.act)
+        D_dx = w.dims[l + 1] * amax(dy_rows) * amax(hi["weights"][l])
+        assert_close(to_f64(s.dx[l])[rows], dx_rows, D_dx, tau, f"dX_{l + 1} (sampled rows)")
+        g_rows, D_g = dx_rows, D_dx
+    for l in range(L):
+        if w.relus[l]:
+            _check_mask_consistency(s, l)
+        _check_adjoint(s, l, tau)
+    return int(touched.sum())
+
+
+@pytest.mark.parametrize("name", ["wide4096x4-f32", "wide4096x4-bf16", "tall512x32768-bf16"])
+def test_full_size_step(name):
+    flips = _check_full_size(name)
+    print(f"{name}: {flips} rows with in-band Relu mask differences")
