@@ -188,10 +188,12 @@ __device__ __forceinline__ void mfma_chunk(f32x16& acc, const u32x4& a, const u3
 
 template <>
 __device__ __forceinline__ void mfma_chunk<float>(f32x16& acc, const u32x4& a, const u32x4& b) {
+  // Reinterpret the whole 16-byte chunk: a bit cast of a single vector
+  // element (a[s]) is lowered by clang to element 0.
+  const f32x4 af = __builtin_bit_cast(f32x4, a);
+  const f32x4 bf = __builtin_bit_cast(f32x4, b);
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__builtin_bit_cast(float, a[s]),
-                                               __builtin_bit_cast(float, b[s]), acc, 0, 0, 0);
+  for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s], bf[s], acc, 0, 0, 0);
 }
 
 template <>

@@ -128,7 +128,7 @@ def test_matmul_identity_and_permutation_bit_exact(layout, dt):
     n = 136
     x_h, x = _host(rng, (264, n), dt)
     perm = rng.permutation(n)
-    P = np.eye(n)[:, perm]
+    P = np.ascontiguousarray(np.eye(n)[:, perm])
     P_dev = torch.from_numpy(P.astype(np.float32)).to(DEV).to(x.dtype)
     out = _empty((264, n), dt)
     if layout == "NN":
