@@ -321,7 +321,8 @@ hipError_t launch_cfg(const GemmDesc& d, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile configuration: 0 = pick by problem size, 1 = 256x256 (4 waves of
+// Tile configuration: 0 = pick by problem size (16-bit operands on whole
+// 256 x 256 tiles go to the direct-to-LDS kernel of gemm_bf16.hip), 1 = 256x256 (4 waves of
 // 128x128), 2 = 256x128 (4 waves of 128x64), 3 = 128x128 (4 waves of 64x64),
 // 4 = 64x64 (4 waves of 32x32). Non-zero values come from the tuning-only
 // environment variable TFD_GEMM_TILE.
@@ -331,7 +332,7 @@ hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t 
   if (tile == 0) {
     const int64_t tiles256 = ((d.m + 255) / 256) * ((d.n + 255) / 256);
     const int64_t tiles128 = ((d.m + 127) / 128) * ((d.n + 127) / 128);
-    tile = tiles256 >= 256 ? 2 : (tiles128 >= 128 ? 3 : 4);
+    tile = tiles256 >= 128 ? 1 : (tiles128 >= 128 ? 3 : 4);
   }
   switch (tile) {
     case 1: return launch_cfg<T, OutT, TA, TB, 256, 256, 2, 2, true>(d, s);
@@ -368,6 +369,7 @@ bool gemm_vector_ok(const GemmDesc& d, int elem_bytes) {
 
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s) {
   const int tile = tile_override();
+  if (tile == 0 && gemm_bf16_256_ok(d)) return launch_gemm_bf16_256(d, s);
   if (d.in_bf16) {
     const bool aligned = gemm_vector_ok(d, 2);
     return d.out_bf16 ? launch_types<bf16, bf16>(d, aligned, tile, s)

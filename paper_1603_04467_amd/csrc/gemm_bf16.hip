@@ -1,0 +1,263 @@
+// MatMul for 16-bit operands on whole 256 x 256 output tiles (the shapes of
+// the wide dense layers), fp32 accumulation, fused bias + ReLU epilogue.
+//
+// Per workgroup: a 256 x 256 output tile, 4 waves each owning 128 x 128
+// (4 x 4 fragments of v_mfma_f32_32x32x16_bf16, 256 accumulators per lane).
+// The k loop walks 64-wide k-tiles through two LDS stages of 64 KiB:
+//  - global -> LDS copies go straight into LDS (global_load_lds_dwordx4, 1 KiB
+//    per wave instruction), so no registers stage them; the copy of k-tile
+//    t+1 is in flight while the matrix cores work on k-tile t;
+//  - an operand that is k-contiguous in memory is kept as 256 rows of 64 k
+//    (128 B rows, 16-byte chunks XOR-swizzled by row) and read with
+//    ds_read_b128: eight consecutive k of one row per lane;
+//  - an operand that is m/n-contiguous in memory is kept as 64 k-rows of 256
+//    values (512 B rows, chunks XOR-swizzled by k) and read with the gfx950
+//    transposing read ds_read_b64_tr_b16, which hands each lane of a 16-lane
+//    group four consecutive k of one column (two reads make the eight k an
+//    MFMA lane needs), so no transpose pass is needed anywhere;
+//  - fragments are double-buffered in registers: the reads for k-step q+1 are
+//    issued before the 16 MFMAs of k-step q.
+// K-slot assignment (identical for both operands, so each k is summed once):
+// lane l supplies k = 32*(l/32) + 8*q + e, e = 0..7, in k-step q of a k-tile.
+//
+// Preconditions (checked by the dispatcher): m, n multiples of 256, k a
+// multiple of 64, 16-byte aligned rows.
+
+#include "common.h"
+#include "kernels.h"
+
+#ifndef TFD_SCHED_GROUPS
+#define TFD_SCHED_GROUPS 1
+#endif
+
+namespace tfd {
+
+namespace {
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+constexpr int kBM = 256, kBN = 256, kBK = 64;
+constexpr int kThreads = 256;
+constexpr int kOperandBytes = 256 * 128;          // one operand's k-tile (32 KiB)
+constexpr int kStageBytes = 2 * kOperandBytes;   // A + B
+
+struct Params {
+  const bf16* a;
+  const bf16* b;
+  void* c;
+  const float* bias;
+  int64_t lda, ldb, ldc;
+  int m, n, k;
+  int epi;
+  int tiles_m, tiles_n;
+};
+
+__device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int swz_mn(int krow) { return (krow & 3) << 2; }
+
+constexpr int kGroupM = 8;
+__device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int total = tiles_m * tiles_n;
+  int t = bid;
+  if (total % kNumXcd == 0) t = (bid % kNumXcd) * (total / kNumXcd) + bid / kNumXcd;
+  const int per_group = kGroupM * tiles_n;
+  const int group = t / per_group;
+  const int first_m = group * kGroupM;
+  const int gsize = min(tiles_m - first_m, kGroupM);
+  const int in_group = t - group * per_group;
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
+
+// Copy one operand's k-tile into LDS. KC: op(X)[mn][k] = X[mn * ld + k];
+// otherwise op(X)[mn][k] = X[k * ld + mn]. Each of the 4 waves issues 8
+// instructions of 64 lanes x 16 bytes; lane i's bytes land at lds + 16 i.
+template <bool KC>
+__device__ __forceinline__ void copy_tile(const bf16* X, int64_t ld, int mn0, int k0, char* lds, int wave,
+                                          int lane) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int blk = wave * 8 + j;  // 1 KiB block of the tile
+    const bf16* g;
+    if (KC) {
+      const int r = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ swz_kc(r);
+      g = X + (int64_t)(mn0 + r) * ld + k0 + c * 8;
+    } else {
+      const int kr = blk * 2 + (lane >> 5);
+      const int c = (lane & 31) ^ swz_mn(kr);
+      g = X + (int64_t)(k0 + kr) * ld + mn0 + c * 8;
+    }
+    __builtin_amdgcn_global_load_lds(g, (lds_void*)(lds + blk * 1024), 16, 0, 0);
+  }
+}
+
+// Fragment of 32 rows (A) or 32 columns (B) starting at `base`, k-step q.
+template <bool KC>
+__device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, int lane) {
+  const int half = lane >> 5;
+  if (KC) {
+    const int r = base + (lane & 31);
+    const int chunk = half * 4 + q;
+    return *reinterpret_cast<const u32x4*>(tile + r * 128 + ((chunk ^ swz_kc(r)) << 4));
+  } else {
+    const int g = lane >> 4, lr = lane & 15;
+    const int mn = base + 16 * (g & 1) + 4 * (lr & 3);
+    const int kb = 32 * half + 8 * q + (lr >> 2);
+    u32x4 out;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int kr = kb + 4 * s;
+      const int off = kr * 512 + (((mn >> 3) ^ swz_mn(kr)) << 4) + (mn & 7) * 2;
+      const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + off));
+      const uint2 u = __builtin_bit_cast(uint2, v);
+      out[2 * s] = u.x;
+      out[2 * s + 1] = u.y;
+    }
+    return out;
+  }
+}
+
+// Scheduling hint: 16 MFMAs spread evenly over kReads groups, each followed
+// by one LDS read.
+template <int T, int kReads>
+__device__ __forceinline__ void interleave_mfma_reads() {
+  if constexpr (T < kReads) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 16 / kReads + (T < 16 % kReads ? 1 : 0), 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    interleave_mfma_reads<T + 1, kReads>();
+  }
+}
+
+template <bool A_KC, bool B_KC, typename OutT>
+__global__ __launch_bounds__(kThreads) void gemm_bf16_256(Params p) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kStageBytes];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int half = lane >> 5, l32 = lane & 31;
+  int tm, tn;
+  tile_of_block(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
+  const int m0 = tm * kBM, n0 = tn * kBN;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int kt_count = p.k / kBK;
+  copy_tile<A_KC>(p.a, p.lda, m0, 0, smem, wave, lane);
+  copy_tile<B_KC>(p.b, p.ldb, n0, 0, smem + kOperandBytes, wave, lane);
+  __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
+  __syncthreads();
+
+  u32x4 fa[2][4], fb[2][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) fa[0][i] = read_frag<A_KC>(smem, wm * 128 + i * 32, 0, lane);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) fb[0][j] = read_frag<B_KC>(smem + kOperandBytes, wn * 128 + j * 32, 0, lane);
+
+  for (int kt = 0; kt < kt_count; ++kt) {
+    const char* st = smem + (kt & 1) * kStageBytes;
+    char* nx = smem + ((kt + 1) & 1) * kStageBytes;
+    const bool more = kt + 1 < kt_count;
+    if (more) {
+      copy_tile<A_KC>(p.a, p.lda, m0, (kt + 1) * kBK, nx, wave, lane);
+      copy_tile<B_KC>(p.b, p.ldb, n0, (kt + 1) * kBK, nx + kOperandBytes, wave, lane);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cb = q & 1, nb = cb ^ 1;
+      if (q < 3) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[nb][i] = read_frag<A_KC>(st, wm * 128 + i * 32, q + 1, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fb[nb][j] = read_frag<B_KC>(st + kOperandBytes, wn * 128 + j * 32, q + 1, lane);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[cb][i]),
+                                                              __builtin_bit_cast(bf16x8, fb[cb][j]),
+                                                              acc[i][j], 0, 0, 0);
+#if TFD_SCHED_GROUPS
+      // Interleave: the next k-step's fragment reads between this k-step's
+      // MFMAs (2 MFMA : 1 LDS read), so their latency hides behind the
+      // matrix cores.
+      // LDS read instructions per k-step: 4 per k-contiguous operand
+      // (ds_read_b128), 8 per m/n-contiguous one (two transposing reads).
+      if (q < 3) interleave_mfma_reads<0, (A_KC ? 4 : 8) + (B_KC ? 4 : 8)>();
+#endif
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (more) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[0][i] = read_frag<A_KC>(nx, wm * 128 + i * 32, 0, lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) fb[0][j] = read_frag<B_KC>(nx + kOperandBytes, wn * 128 + j * 32, 0, lane);
+    }
+  }
+
+  OutT* C = static_cast<OutT*>(p.c);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = n0 + wn * 128 + j * 32 + l32;
+    const float bv = p.epi != 0 ? p.bias[col] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        float v = acc[i][j][r] + bv;
+        if (p.epi == 2) v = relu_f32(v);
+        store_from_f32(C + (int64_t)row * p.ldc + col, v);
+      }
+    }
+  }
+}
+
+template <bool A_KC, bool B_KC>
+hipError_t launch(const GemmDesc& d, hipStream_t s) {
+  Params p;
+  p.a = static_cast<const bf16*>(d.a);
+  p.b = static_cast<const bf16*>(d.b);
+  p.c = d.c;
+  p.bias = d.bias;
+  p.lda = d.lda;
+  p.ldb = d.ldb;
+  p.ldc = d.ldc;
+  p.m = (int)d.m;
+  p.n = (int)d.n;
+  p.k = (int)d.k;
+  p.epi = d.epi;
+  p.tiles_m = p.m / kBM;
+  p.tiles_n = p.n / kBN;
+  dim3 grid(p.tiles_m * p.tiles_n), block(kThreads);
+  if (d.out_bf16)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16>), grid, block, 0, s, p);
+  else
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float>), grid, block, 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool gemm_bf16_256_ok(const GemmDesc& d) {
+  return d.in_bf16 && d.m % kBM == 0 && d.n % kBN == 0 && d.k % kBK == 0 && d.k > 0 &&
+         gemm_vector_ok(d, 2) && !(d.ta && d.tb);
+}
+
+hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
+  // A is k-contiguous unless transposed; B is k-contiguous when transposed.
+  if (!d.ta && !d.tb) return launch<true, false>(d, s);
+  if (!d.ta && d.tb) return launch<true, true>(d, s);
+  return launch<false, false>(d, s);
+}
+
+}  // namespace tfd

@@ -112,6 +112,30 @@ def test_matmul_every_tile_config(tile, layout, din, dout):
     assert_close(got, want, D, TAU[din], f"tile {tile} {layout} {din}->{dout}")
 
 
+WHOLE_TILES = [(256, 256, 64), (512, 768, 192), (768, 512, 1024), (1024, 256, 4096)]
+
+
+@pytest.mark.parametrize("epi", ["none", "bias", "bias_relu"])
+@pytest.mark.parametrize("dout", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("m,n,k", WHOLE_TILES)
+def test_matmul_bf16_whole_tiles(m, n, k, layout, dout, epi):
+    """16-bit operands on whole 256 x 256 tiles (the direct-to-LDS kernel)."""
+    got, want, pre, D = _run_gemm(m, n, k, layout, "bf16", dout, epi, seed=k)
+    assert_close(got, want, D, TAU["bf16"], f"{layout} bf16->{dout} {m}x{n}x{k} {epi}")
+    if epi == "bias_relu":
+        bad, _ = mask_mismatch(got, pre, TAU["bf16"] * D)
+        assert bad == 0
+
+
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_matmul_bf16_whole_tiles_integers_exact(layout):
+    got, want, _, _ = _run_gemm(512, 512, 64, layout, "bf16", "bf16", "none", kind="int")
+    assert_bits(got, want, f"integer whole tiles {layout}")
+    got, want, _, _ = _run_gemm(512, 256, 128, layout, "bf16", "f32", "none", kind="int")
+    assert_bits(got, want, f"integer whole tiles {layout} f32 out")
+
+
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 @pytest.mark.parametrize("din", ["f32", "bf16"])
 def test_matmul_small_integers_exact(layout, din):
@@ -123,14 +147,14 @@ def test_matmul_small_integers_exact(layout, din):
 
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_matmul_identity_and_permutation_bit_exact(layout, dt):
+@pytest.mark.parametrize("rows,n", [(264, 136), (512, 256)])
+def test_matmul_identity_and_permutation_bit_exact(layout, dt, rows, n):
     rng = np.random.default_rng(9)
-    n = 136
-    x_h, x = _host(rng, (264, n), dt)
+    x_h, x = _host(rng, (rows, n), dt)
     perm = rng.permutation(n)
     P = np.ascontiguousarray(np.eye(n)[:, perm])
     P_dev = torch.from_numpy(P.astype(np.float32)).to(DEV).to(x.dtype)
-    out = _empty((264, n), dt)
+    out = _empty((rows, n), dt)
     if layout == "NN":
         T.tfd_matmul(x, P_dev, out)                                   # x @ P
         want = x_h[:, perm]
