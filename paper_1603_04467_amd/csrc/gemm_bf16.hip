@@ -26,10 +26,6 @@
 #include "common.h"
 #include "kernels.h"
 
-#ifndef TFD_SCHED_GROUPS
-#define TFD_SCHED_GROUPS 1
-#endif
-
 namespace tfd {
 
 namespace {
@@ -185,14 +181,11 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_256(Params p) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[cb][i]),
                                                               __builtin_bit_cast(bf16x8, fb[cb][j]),
                                                               acc[i][j], 0, 0, 0);
-#if TFD_SCHED_GROUPS
-      // Interleave: the next k-step's fragment reads between this k-step's
-      // MFMAs (2 MFMA : 1 LDS read), so their latency hides behind the
-      // matrix cores.
-      // LDS read instructions per k-step: 4 per k-contiguous operand
-      // (ds_read_b128), 8 per m/n-contiguous one (two transposing reads).
+      // Interleave the next k-step's fragment reads between this k-step's
+      // MFMAs so their latency hides behind the matrix cores. LDS read
+      // instructions per k-step: 4 per k-contiguous operand (ds_read_b128),
+      // 8 per m/n-contiguous one (two transposing reads).
       if (q < 3) interleave_mfma_reads<0, (A_KC ? 4 : 8) + (B_KC ? 4 : 8)>();
-#endif
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();

@@ -78,8 +78,10 @@ __device__ __forceinline__ float masked(float g, float f) {
 }
 
 template <typename T, bool MASK, bool WRITE, bool VEC>
-__global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* g, const T* f, T* out,
-                                                                  float* partial, int64_t rows,
+__global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __restrict__ g,
+                                                                  const T* __restrict__ f,
+                                                                  T* __restrict__ out,
+                                                                  float* __restrict__ partial, int64_t rows,
                                                                   int64_t cols, int64_t rows_per_chunk) {
   constexpr int V = Chunk16<T>::V;
   __shared__ float sh[kRowPhases][kColChunks * V];
@@ -96,7 +98,32 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* g, co
 
   if (c0 < cols) {
     const bool full = VEC && (c0 + V <= cols);
-    for (int64_t r = r_begin + phase; r < r_end; r += kRowPhases) {
+    int64_t r = r_begin + phase;
+    if (full) {
+      // four rows per round: all loads issued before the ordered additions
+      constexpr int U = 4;
+      for (; r + (U - 1) * kRowPhases < r_end; r += U * kRowPhases) {
+        float x[U][V];
+#pragma unroll
+        for (int u = 0; u < U; ++u) Chunk16<T>::load(g + (r + u * kRowPhases) * cols + c0, x[u]);
+        if (MASK) {
+          float m[U][V];
+#pragma unroll
+          for (int u = 0; u < U; ++u) Chunk16<T>::load(f + (r + u * kRowPhases) * cols + c0, m[u]);
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < V; ++e) x[u][e] = masked(x[u][e], m[u][e]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          if (WRITE) Chunk16<T>::store(out + (r + u * kRowPhases) * cols + c0, x[u]);
+#pragma unroll
+          for (int e = 0; e < V; ++e) acc[e] += x[u][e];
+        }
+      }
+    }
+    for (; r < r_end; r += kRowPhases) {
       const int64_t base = r * cols + c0;
       float x[V];
       if (full) {
@@ -137,12 +164,24 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* g, co
   }
 }
 
+// Sums the row-chunk partials of each column in chunk order. The loads are
+// independent of the running sum, so they are issued kBatch at a time before
+// the (ordered) additions.
 __global__ __launch_bounds__(kThreads) void colsum_final_kernel(const float* partial, float* db,
                                                                 int64_t row_chunks, int64_t cols) {
+  constexpr int kBatch = 16;
   const int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (c >= cols) return;
   float s = 0.0f;
-  for (int64_t k = 0; k < row_chunks; ++k) s += partial[k * cols + c];
+  int64_t k = 0;
+  for (; k + kBatch <= row_chunks; k += kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) v[u] = partial[(k + u) * cols + c];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) s += v[u];
+  }
+  for (; k < row_chunks; ++k) s += partial[k * cols + c];
   db[c] = s;
 }
 
