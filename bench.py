@@ -39,6 +39,14 @@ PRIMARY = "wide4096x4-bf16"
 SECONDARY = "wide4096x4-f32"
 
 
+def _gemm_bytes(shape, layout, eb):
+    """Compulsory HBM bytes of one GEMM: read A and B once, write C once
+    (the weight gradient is written in fp32)."""
+    m, n, k = shape
+    out = 4 if layout == "TN" else eb
+    return m * k * eb + k * n * eb + m * n * out
+
+
 def _op_kind(name: str) -> str:
     for p in ("fwd", "dx", "dw", "relugrad", "sgd", "loss"):
         if name.startswith(p):
@@ -132,6 +140,8 @@ def time_workload(name: str, steps: int, warmup: int):
     dom_flops = dom[0]["flops"]
     achieved = dom_flops / (dom_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.act]
+    kernel_name = f"gemm_{dom_layout}_{w.act}"
+    traffic = lookup_traffic(kernel_name, dom[0]["shape"], w.act)
     return {
         "workload": w,
         "ms": ms,
@@ -141,16 +151,50 @@ def time_workload(name: str, steps: int, warmup: int):
         "ops": ops,
         "roofline": {
             "bound": "mfma",
-            "kernel": f"gemm_{dom_layout}_{w.act}",
+            "kernel": kernel_name,
             "shape": dom[0]["shape"],
             "achieved": achieved,
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": achieved / peak,
-            "traffic": None,
+            "traffic": None if traffic is None else traffic["bytes"],
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
+            "algorithmic_bytes": _gemm_bytes(dom[0]["shape"], dom_layout, eb),
+            "src": KERNEL_SOURCES[w.act],
         },
         "loss": float(s.loss.item()),
     }
+
+
+# HBM traffic of the dominant kernel, from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE
+# runs summarised under profiles/. A record applies only while the kernel's
+# source file is unchanged (its sha256 is part of the record).
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.md")
+KERNEL_SOURCES = {"bf16": "paper_1603_04467_amd/csrc/gemm_bf16.hip", "f32": "paper_1603_04467_amd/csrc/gemm.hip"}
+
+
+def _sha256(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def lookup_traffic(kernel: str, shape, dtype: str):
+    """Bytes per launch (FETCH_SIZE and WRITE_SIZE, each scaled by its
+    calibration factor) recorded for `kernel` at `shape`, or None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    src = _sha256(os.path.join(ROOT, KERNEL_SOURCES[dtype]))
+    want = f"{shape[0]}x{shape[1]}x{shape[2]}"
+    for line in open(TRAFFIC_FILE):
+        if not line.startswith("record "):
+            continue
+        kv = dict(item.split("=", 1) for item in line.split()[1:])
+        if kv.get("kernel") == kernel and kv.get("shape") == want and kv.get("src_sha256") == src:
+            fetch = float(kv["fetch_kib"]) * float(kv["fetch_scale"]) * 1024
+            write = float(kv["write_kib"]) * float(kv["write_scale"]) * 1024
+            return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write}
+    return None
 
 
 def cpu_baseline(name: str, rows: int):
@@ -185,6 +229,19 @@ def cpu_baseline(name: str, rows: int):
     }
 
 
+def _per_op(ops):
+    """Mean ms per op, with TFLOP/s (GEMMs) or GB/s (memory-bound ops)."""
+    out = {}
+    for k, v in ops.items():
+        d = {"ms": round(v["ms"], 4)}
+        if "tflops" in v:
+            d["tflops"] = round(v["tflops"], 1)
+        if "gbs" in v:
+            d["gbs"] = round(v["gbs"], 1)
+        out[k] = d
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -193,7 +250,7 @@ def main():
     ap.add_argument("--workload", default=PRIMARY)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--cpu-rows", type=int, default=8192)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -235,7 +292,7 @@ def main():
         },
         "pct_mfma_peak": round(r["pct_peak"], 2),
         "roofline": r["roofline"],
-        "per_op_ms": {k: round(v["ms"], 4) for k, v in r["ops"].items()},
+        "per_op": _per_op(r["ops"]),
         "loss": r["loss"],
     }
     if not args.no_secondary and args.workload == PRIMARY:
@@ -248,7 +305,7 @@ def main():
             "ms_per_step": round(r2["ms"], 4),
             "pct_mfma_peak": round(r2["pct_peak"], 2),
             "roofline": r2["roofline"],
-            "per_op_ms": {k: round(v["ms"], 4) for k, v in r2["ops"].items()},
+            "per_op": _per_op(r2["ops"]),
         }
     if not args.no_cpu_baseline:
         print(f"bench: timing the oracle on {args.cpu_rows} rows", file=sys.stderr, flush=True)
