@@ -123,7 +123,9 @@ def time_workload(name: str, steps: int, warmup: int):
             d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
         elif kind == "sgd":
             K, M = w.dims[l - 1], w.dims[l]
-            byt = K * M * (12 + (2 if w.masters else 0)) + 12 * M
+            # fp32 var and delta read, var written; with fp32 masters also the
+            # 16-bit copy and its transpose (2 + 2 bytes); the bias update
+            byt = K * M * (12 + (4 if w.masters else 0)) + 12 * M
             d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
         elif kind == "loss":
             byt = 3 * N * w.dims[-1] * eb

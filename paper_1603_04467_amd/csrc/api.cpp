@@ -233,4 +233,20 @@ tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delt
                     "tfd_apply_gradient_descent launch");
 }
 
+tfd_status tfd_apply_gradient_descent_matrix(float* var, float alpha, const float* delta, int64_t rows,
+                                             int64_t cols, uint16_t* var_bf16, uint16_t* var_bf16_t,
+                                             void* stream) {
+  g_err[0] = 0;
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: negative size");
+  if (rows == 0 || cols == 0) return TFD_OK;
+  if (!var || !delta) return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: NULL pointer");
+  const size_t n = (size_t)rows * (size_t)cols;
+  if (overlaps(var, n * 4, delta, n * 4) || overlaps(var_bf16, n * 2, var, n * 4) ||
+      overlaps(var_bf16, n * 2, delta, n * 4) || overlaps(var_bf16_t, n * 2, var, n * 4) ||
+      overlaps(var_bf16_t, n * 2, delta, n * 4) || overlaps(var_bf16, n * 2, var_bf16_t, n * 2))
+    return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: overlapping buffers");
+  return hip_status(tfd::launch_sgd_matrix(var, alpha, delta, rows, cols, var_bf16, var_bf16_t, as_stream(stream)),
+                    "tfd_apply_gradient_descent_matrix launch");
+}
+
 }  // extern "C"

@@ -233,7 +233,91 @@ __global__ __launch_bounds__(kThreads) void sgd_kernel(float* var, float alpha, 
   }
 }
 
+// ApplyGradientDescent on a weight matrix, refreshing its 16-bit operand
+// copies: 64 x 64 tiles, one block each. The updated tile's 16-bit bits are
+// staged in LDS so that the transposed copy is also written in 16-byte row
+// chunks. VEC: whole tiles with 16-byte aligned rows (else per-element).
+constexpr int kSgdTile = 64;
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict__ var, float alpha,
+                                                              const float* __restrict__ delta, int64_t rows,
+                                                              int64_t cols, uint16_t* __restrict__ shadow,
+                                                              uint16_t* __restrict__ shadow_t) {
+  __shared__ uint16_t tile[kSgdTile][kSgdTile + 2];
+  const int64_t r0 = (int64_t)blockIdx.y * kSgdTile, c0 = (int64_t)blockIdx.x * kSgdTile;
+  const int tid = threadIdx.x;
+  const float na = -alpha;
+  const bool full = VEC && r0 + kSgdTile <= rows && c0 + kSgdTile <= cols;
+  if (full) {
+    const int cc = (tid & 15) * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = (tid >> 4) + 16 * i;
+      const int64_t off = (r0 + rr) * cols + c0 + cc;
+      f32x4 v = *reinterpret_cast<const f32x4*>(var + off);
+      const f32x4 d = *reinterpret_cast<const f32x4*>(delta + off);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = __builtin_fmaf(na, d[e], v[e]);
+      *reinterpret_cast<f32x4*>(var + off) = v;
+      uint16_t b[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        b[e] = bf16_bits(v[e]);
+        tile[rr][cc + e] = b[e];
+      }
+      if (shadow)
+        *reinterpret_cast<uint2*>(shadow + off) =
+            make_uint2((uint32_t)b[0] | ((uint32_t)b[1] << 16), (uint32_t)b[2] | ((uint32_t)b[3] << 16));
+    }
+  } else {
+    for (int i = tid; i < kSgdTile * kSgdTile; i += kThreads) {
+      const int rr = i / kSgdTile, cc = i % kSgdTile;
+      const int64_t r = r0 + rr, c = c0 + cc;
+      if (r < rows && c < cols) {
+        const int64_t off = r * cols + c;
+        const float v = __builtin_fmaf(na, delta[off], var[off]);
+        var[off] = v;
+        const uint16_t b = bf16_bits(v);
+        tile[rr][cc] = b;
+        if (shadow) shadow[off] = b;
+      }
+    }
+  }
+  if (!shadow_t) return;
+  __syncthreads();
+  // transposed copy: output row c (= input column), 64 input rows per tile
+  if (full && (rows % 8) == 0) {
+    const int oc = tid >> 2, seg = (tid & 3) * 16;
+    uint32_t w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      w[e] = (uint32_t)tile[seg + 2 * e][oc] | ((uint32_t)tile[seg + 2 * e + 1][oc] << 16);
+    uint16_t* dst = shadow_t + (c0 + oc) * rows + r0 + seg;
+    *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4*>(dst + 8) = u32x4{w[4], w[5], w[6], w[7]};
+  } else {
+    for (int i = tid; i < kSgdTile * kSgdTile; i += kThreads) {
+      const int oc = i / kSgdTile, rr = i % kSgdTile;
+      const int64_t r = r0 + rr, c = c0 + oc;
+      if (r < rows && c < cols) shadow_t[c * rows + r] = tile[rr][oc];
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,
+                             uint16_t* shadow, uint16_t* shadow_t, hipStream_t s) {
+  const bool vec = aligned16(var) && aligned16(delta) && cols % 4 == 0 &&
+                   ((reinterpret_cast<uintptr_t>(shadow) & 7) == 0) && aligned16(shadow_t);
+  dim3 grid((unsigned)((cols + kSgdTile - 1) / kSgdTile), (unsigned)((rows + kSgdTile - 1) / kSgdTile));
+  if (vec)
+    hipLaunchKernelGGL((sgd_matrix_kernel<true>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow, shadow_t);
+  else
+    hipLaunchKernelGGL((sgd_matrix_kernel<false>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow, shadow_t);
+  return hipGetLastError();
+}
 
 hipError_t launch_bias_add(const void* value, const float* bias, void* out, int64_t rows, int64_t cols,
                            bool bf16_t, hipStream_t s) {

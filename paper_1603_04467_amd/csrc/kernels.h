@@ -48,5 +48,7 @@ hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, 
 
 hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow,
                       hipStream_t s);
+hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,
+                             uint16_t* shadow, uint16_t* shadow_t, hipStream_t s);
 
 }  // namespace tfd

@@ -46,6 +46,13 @@ class DenseStep:
         self.weights = [_to_device(a, w.act, dev) for a in inputs["weights"]]
         self.masters = None if inputs["masters"] is None else [_to_device(a, "f32", dev) for a in inputs["masters"]]
         self.biases = [_to_device(a, "f32", dev) for a in inputs["biases"]]
+        # With fp32 masters, the 16-bit weights are kept twice: W [fan_in, fan_out]
+        # for the input-gradient MatMul and W^T [fan_out, fan_in] so that the
+        # forward MatMul reads its weight operand k-contiguous (transpose_b).
+        # Both copies are refreshed by the update kernel.
+        self.weights_t = None
+        if self.masters is not None:
+            self.weights_t = [torch.empty(w.dims[l + 1], w.dims[l], dtype=self.act, device=dev) for l in range(L)]
         self.target = None if inputs["target"] is None else _to_device(inputs["target"], w.act, dev)
         self.upstream = None if inputs["upstream"] is None else _to_device(inputs["upstream"], w.act, dev)
 
@@ -62,6 +69,13 @@ class DenseStep:
         need.append(T.tfd_loss_workspace_size(N * w.dims[-1], self.act))
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
+        if self.weights_t is not None:
+            # derive W^T from the masters with the update kernel (alpha = 0)
+            for l in range(L):
+                self.dw[l].zero_()
+                T.tfd_apply_gradient_descent_matrix(self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
+                                                    var_bf16_t=self.weights_t[l])
+
         # pristine copies of the Variables, to restart from the same state
         self._saved = [t.clone() for t in self.variables()]
 
@@ -69,6 +83,8 @@ class DenseStep:
         out = list(self.weights) + list(self.biases)
         if self.masters is not None:
             out += list(self.masters)
+        if self.weights_t is not None:
+            out += list(self.weights_t)
         return out
 
     def restore(self):
@@ -84,8 +100,12 @@ class DenseStep:
         for l in range(L):
             if mark:
                 mark(f"fwd{l + 1}")
-            T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l],
-                         epilogue="bias_relu" if w.relus[l] else "bias")
+            epi = "bias_relu" if w.relus[l] else "bias"
+            if self.weights_t is not None:
+                T.tfd_matmul(self.h[l], self.weights_t[l], self.h[l + 1], transpose_b=True, bias=self.biases[l],
+                             epilogue=epi)
+            else:
+                T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l], epilogue=epi)
         if self.upstream is None:
             if mark:
                 mark("loss")
@@ -110,7 +130,8 @@ class DenseStep:
                 if mark:
                     mark(f"sgd{l + 1}")
                 if self.masters is not None:
-                    T.tfd_apply_gradient_descent(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l])
+                    T.tfd_apply_gradient_descent_matrix(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l],
+                                                        var_bf16_t=self.weights_t[l])
                 else:
                     T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l])
                 T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l])

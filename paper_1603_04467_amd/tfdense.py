@@ -29,7 +29,7 @@ EXPORTS = (
     "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
     "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
     "tfd_relu_grad_bias_add_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
-    "tfd_apply_gradient_descent",
+    "tfd_apply_gradient_descent", "tfd_apply_gradient_descent_matrix",
 )
 
 
@@ -66,6 +66,7 @@ def load() -> ctypes.CDLL:
         "tfd_loss_workspace_size": ([i64, i32], sz),
         "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
         "tfd_apply_gradient_descent": ([vp, ctypes.c_float, vp, i64, vp, vp], i32),
+        "tfd_apply_gradient_descent_matrix": ([vp, ctypes.c_float, vp, i64, i64, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -205,4 +206,20 @@ def tfd_apply_gradient_descent(var, alpha, delta, var_bf16=None, stream=None):
         raise TypeError("the 16-bit copy must be bfloat16")
     _check(load().tfd_apply_gradient_descent(_ptr(var), float(alpha), _ptr(delta), n, _ptr(var_bf16),
                                              _stream(stream)))
+    return var
+
+
+def tfd_apply_gradient_descent_matrix(var, alpha, delta, var_bf16=None, var_bf16_t=None, stream=None):
+    """var[rows, cols] -= alpha * delta (one rounding), refreshing the 16-bit
+    copies var_bf16 [rows, cols] and var_bf16_t [cols, rows] when given."""
+    if var.dim() != 2 or not var.is_contiguous() or var.dtype != torch.float32:
+        raise ValueError("var must be a contiguous fp32 matrix")
+    if delta.shape != var.shape or delta.dtype != torch.float32 or not delta.is_contiguous():
+        raise ValueError("delta must match var")
+    rows, cols = var.shape
+    for t, shape in ((var_bf16, (rows, cols)), (var_bf16_t, (cols, rows))):
+        if t is not None and (t.dtype != torch.bfloat16 or tuple(t.shape) != shape or not t.is_contiguous()):
+            raise ValueError("16-bit copies must be contiguous bfloat16 of the matching shape")
+    _check(load().tfd_apply_gradient_descent_matrix(_ptr(var), float(alpha), _ptr(delta), rows, cols,
+                                                    _ptr(var_bf16), _ptr(var_bf16_t), _stream(stream)))
     return var

@@ -255,6 +255,28 @@ def test_apply_gradient_descent_bit_exact(count, shadow):
         assert_bits(to_f64(sh), oracle.round_bf16(want), "sgd shadow")
 
 
+@pytest.mark.parametrize("rows,cols", [(1, 1), (3, 5), (64, 64), (100, 37), (130, 72), (512, 768), (4096, 4096)])
+def test_apply_gradient_descent_matrix_bit_exact(rows, cols):
+    rng = np.random.default_rng([rows, cols])
+    var = rng.standard_normal((rows, cols)).astype(np.float32)
+    delta = (rng.standard_normal((rows, cols)) * 10.0 ** rng.integers(-6, 4, (rows, cols))).astype(np.float32)
+    v = torch.from_numpy(var).to(DEV)
+    d = torch.from_numpy(delta).to(DEV)
+    sh = torch.empty(rows, cols, dtype=torch.bfloat16, device=DEV)
+    sht = torch.empty(cols, rows, dtype=torch.bfloat16, device=DEV)
+    T.tfd_apply_gradient_descent_matrix(v, 0.01, d, var_bf16=sh, var_bf16_t=sht)
+    torch.cuda.synchronize()
+    want = oracle.apply_gradient_descent(var, np.float32(0.01), delta)
+    assert_bits(to_f64(v), want, "sgd matrix")
+    assert_bits(to_f64(sh), oracle.round_bf16(want), "sgd matrix copy")
+    assert_bits(to_f64(sht), oracle.round_bf16(want).T, "sgd matrix transposed copy")
+    # copies are optional
+    v2 = torch.from_numpy(var).to(DEV)
+    T.tfd_apply_gradient_descent_matrix(v2, 0.01, d)
+    torch.cuda.synchronize()
+    assert torch.equal(v, v2)
+
+
 def test_apply_gradient_descent_lr_zero_is_identity():
     var = torch.randn(12345, device=DEV)
     keep = var.clone()
