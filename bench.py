@@ -112,6 +112,7 @@ def time_workload(name: str, steps: int, warmup: int):
         if kind in ("fwd", "dx", "dw"):
             if kind == "fwd":
                 m, n, k, lay = gemm_shapes[l - 1]
+                lay = s.forward_layout
             else:
                 idx = L + 2 * (L - l) + (0 if kind == "dx" else 1)
                 m, n, k, lay = gemm_shapes[idx]
@@ -252,7 +253,7 @@ def main():
     ap.add_argument("--workload", default=PRIMARY)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=8192)
+    ap.add_argument("--cpu-rows", type=int, default=16384)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

@@ -23,6 +23,9 @@
 // Preconditions (checked by the dispatcher): m, n multiples of 256, k a
 // multiple of 64, 16-byte aligned rows.
 
+#include <stdlib.h>
+#include <string.h>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -35,7 +38,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kThreads = 256;
+
 constexpr int kOperandBytes = 256 * 128;          // one operand's k-tile (32 KiB)
 constexpr int kStageBytes = 2 * kOperandBytes;   // A + B
 
@@ -70,12 +73,13 @@ __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n,
 // Copy one operand's k-tile into LDS. KC: op(X)[mn][k] = X[mn * ld + k];
 // otherwise op(X)[mn][k] = X[k * ld + mn]. Each of the 4 waves issues 8
 // instructions of 64 lanes x 16 bytes; lane i's bytes land at lds + 16 i.
-template <bool KC>
+template <bool KC, int kThreads>
 __device__ __forceinline__ void copy_tile(const bf16* X, int64_t ld, int mn0, int k0, char* lds, int wave,
                                           int lane) {
+  constexpr int kPerWave = 32 / (kThreads / 64);  // 1 KiB blocks per wave
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int blk = wave * 8 + j;  // 1 KiB block of the tile
+  for (int j = 0; j < kPerWave; ++j) {
+    const int blk = wave * kPerWave + j;  // 1 KiB block of the tile
     const bf16* g;
     if (KC) {
       const int r = blk * 8 + (lane >> 3);
@@ -118,66 +122,69 @@ __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, in
 
 // Scheduling hint: 16 MFMAs spread evenly over kReads groups, each followed
 // by one LDS read.
-template <int T, int kReads>
+template <int T, int kReads, int kMfma>
 __device__ __forceinline__ void interleave_mfma_reads() {
   if constexpr (T < kReads) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 16 / kReads + (T < 16 % kReads ? 1 : 0), 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma / kReads + (T < kMfma % kReads ? 1 : 0), 0);
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    interleave_mfma_reads<T + 1, kReads>();
+    interleave_mfma_reads<T + 1, kReads, kMfma>();
   }
 }
 
-template <bool A_KC, bool B_KC, typename OutT>
-__global__ __launch_bounds__(kThreads) void gemm_bf16_256(Params p) {
+template <bool A_KC, bool B_KC, typename OutT, int kWavesM, int kWavesN>
+__global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p) {
+  constexpr int kThreads = 64 * kWavesM * kWavesN;
+  constexpr int kFM = kBM / kWavesM / 32, kFN = kBN / kWavesN / 32;  // fragments per wave
   __shared__ __attribute__((aligned(1024))) char smem[2 * kStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / kWavesN, wn = wave % kWavesN;
+  constexpr int kWTM = kBM / kWavesM, kWTN = kBN / kWavesN;  // wave tile
   const int half = lane >> 5, l32 = lane & 31;
   int tm, tn;
   tile_of_block(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
 
-  f32x16 acc[4][4];
+  f32x16 acc[kFM][kFN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kFM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kFN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int kt_count = p.k / kBK;
-  copy_tile<A_KC>(p.a, p.lda, m0, 0, smem, wave, lane);
-  copy_tile<B_KC>(p.b, p.ldb, n0, 0, smem + kOperandBytes, wave, lane);
+  copy_tile<A_KC, kThreads>(p.a, p.lda, m0, 0, smem, wave, lane);
+  copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, 0, smem + kOperandBytes, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
   __syncthreads();
 
-  u32x4 fa[2][4], fb[2][4];
+  u32x4 fa[2][kFM], fb[2][kFN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) fa[0][i] = read_frag<A_KC>(smem, wm * 128 + i * 32, 0, lane);
+  for (int i = 0; i < kFM; ++i) fa[0][i] = read_frag<A_KC>(smem, wm * kWTM + i * 32, 0, lane);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) fb[0][j] = read_frag<B_KC>(smem + kOperandBytes, wn * 128 + j * 32, 0, lane);
+  for (int j = 0; j < kFN; ++j) fb[0][j] = read_frag<B_KC>(smem + kOperandBytes, wn * kWTN + j * 32, 0, lane);
 
   for (int kt = 0; kt < kt_count; ++kt) {
     const char* st = smem + (kt & 1) * kStageBytes;
     char* nx = smem + ((kt + 1) & 1) * kStageBytes;
     const bool more = kt + 1 < kt_count;
     if (more) {
-      copy_tile<A_KC>(p.a, p.lda, m0, (kt + 1) * kBK, nx, wave, lane);
-      copy_tile<B_KC>(p.b, p.ldb, n0, (kt + 1) * kBK, nx + kOperandBytes, wave, lane);
+      copy_tile<A_KC, kThreads>(p.a, p.lda, m0, (kt + 1) * kBK, nx, wave, lane);
+      copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, (kt + 1) * kBK, nx + kOperandBytes, wave, lane);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int cb = q & 1, nb = cb ^ 1;
       if (q < 3) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) fa[nb][i] = read_frag<A_KC>(st, wm * 128 + i * 32, q + 1, lane);
+        for (int i = 0; i < kFM; ++i) fa[nb][i] = read_frag<A_KC>(st, wm * kWTM + i * 32, q + 1, lane);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) fb[nb][j] = read_frag<B_KC>(st + kOperandBytes, wn * 128 + j * 32, q + 1, lane);
+        for (int j = 0; j < kFN; ++j) fb[nb][j] = read_frag<B_KC>(st + kOperandBytes, wn * kWTN + j * 32, q + 1, lane);
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kFM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kFN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[cb][i]),
                                                               __builtin_bit_cast(bf16x8, fb[cb][j]),
                                                               acc[i][j], 0, 0, 0);
@@ -185,28 +192,28 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_256(Params p) {
       // MFMAs so their latency hides behind the matrix cores. LDS read
       // instructions per k-step: 4 per k-contiguous operand (ds_read_b128),
       // 8 per m/n-contiguous one (two transposing reads).
-      if (q < 3) interleave_mfma_reads<0, (A_KC ? 4 : 8) + (B_KC ? 4 : 8)>();
+      if (q < 3) interleave_mfma_reads<0, kFM * (A_KC ? 1 : 2) + kFN * (B_KC ? 1 : 2), kFM * kFN>();
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (more) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[0][i] = read_frag<A_KC>(nx, wm * 128 + i * 32, 0, lane);
+      for (int i = 0; i < kFM; ++i) fa[0][i] = read_frag<A_KC>(nx, wm * kWTM + i * 32, 0, lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[0][j] = read_frag<B_KC>(nx + kOperandBytes, wn * 128 + j * 32, 0, lane);
+      for (int j = 0; j < kFN; ++j) fb[0][j] = read_frag<B_KC>(nx + kOperandBytes, wn * kWTN + j * 32, 0, lane);
     }
   }
 
   OutT* C = static_cast<OutT*>(p.c);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int col = n0 + wn * 128 + j * 32 + l32;
+  for (int j = 0; j < kFN; ++j) {
+    const int col = n0 + wn * kWTN + j * 32 + l32;
     const float bv = p.epi != 0 ? p.bias[col] : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kFM; ++i) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const int row = m0 + wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         float v = acc[i][j][r] + bv;
         if (p.epi == 2) v = relu_f32(v);
         store_from_f32(C + (int64_t)row * p.ldc + col, v);
@@ -215,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_256(Params p) {
   }
 }
 
-template <bool A_KC, bool B_KC>
+template <bool A_KC, bool B_KC, int WM, int WN>
 hipError_t launch(const GemmDesc& d, hipStream_t s) {
   Params p;
   p.a = static_cast<const bf16*>(d.a);
@@ -231,12 +238,30 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.epi = d.epi;
   p.tiles_m = p.m / kBM;
   p.tiles_n = p.n / kBN;
-  dim3 grid(p.tiles_m * p.tiles_n), block(kThreads);
+  dim3 grid(p.tiles_m * p.tiles_n), block(64 * WM * WN);
   if (d.out_bf16)
-    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float, WM, WN>), grid, block, 0, s, p);
   return hipGetLastError();
+}
+
+// Waves per workgroup: 4 (2x2 of 128x128), 8 (2x4 of 128x64) or 16 (4x4 of 64x64).
+template <bool A_KC, bool B_KC>
+hipError_t launch_waves(const GemmDesc& d, int waves, hipStream_t s) {
+  if (waves == 4) return launch<A_KC, B_KC, 2, 2>(d, s);
+  if (waves == 16) return launch<A_KC, B_KC, 4, 4>(d, s);
+  return launch<A_KC, B_KC, 2, 4>(d, s);
+}
+
+// Tuning-only override "NN:8,NT:4,TN:16" (environment variable TFD_BF16_WAVES).
+int waves_for(const char* layout, int dflt) {
+  const char* e = getenv("TFD_BF16_WAVES");
+  if (!e) return dflt;
+  const char* f = strstr(e, layout);
+  if (!f) return dflt;
+  const int v = atoi(f + 3);
+  return (v == 4 || v == 8 || v == 16) ? v : dflt;
 }
 
 }  // namespace
@@ -248,9 +273,12 @@ bool gemm_bf16_256_ok(const GemmDesc& d) {
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // A is k-contiguous unless transposed; B is k-contiguous when transposed.
-  if (!d.ta && !d.tb) return launch<true, false>(d, s);
-  if (!d.ta && d.tb) return launch<true, true>(d, s);
-  return launch<false, false>(d, s);
+  // Defaults measured inside the training step: 8 waves (2 per SIMD) for
+  // NN and NT, 16 waves for TN, whose two transposing-read operands gain most
+  // from more waves to hide LDS latency.
+  if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for("NN", 8), s);
+  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for("NT", 8), s);
+  return launch_waves<false, false>(d, waves_for("TN", 16), s);
 }
 
 }  // namespace tfd

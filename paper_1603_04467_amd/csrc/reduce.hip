@@ -21,7 +21,13 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kColChunks = 64;               // column chunks per block
 constexpr int kRowPhases = kThreads / kColChunks;
-constexpr int kTargetBlocks = 2048;
+#ifndef TFD_REDUCE_BLOCKS
+#define TFD_REDUCE_BLOCKS 2048
+#endif
+#ifndef TFD_REDUCE_UNROLL
+#define TFD_REDUCE_UNROLL 4
+#endif
+constexpr int kTargetBlocks = TFD_REDUCE_BLOCKS;
 
 struct ReducePlan {
   int64_t col_groups, row_chunks, rows_per_chunk;
@@ -101,7 +107,7 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
     int64_t r = r_begin + phase;
     if (full) {
       // four rows per round: all loads issued before the ordered additions
-      constexpr int U = 4;
+      constexpr int U = TFD_REDUCE_UNROLL;
       for (; r + (U - 1) * kRowPhases < r_end; r += U * kRowPhases) {
         float x[U][V];
 #pragma unroll

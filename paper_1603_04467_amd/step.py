@@ -53,6 +53,8 @@ class DenseStep:
         self.weights_t = None
         if self.masters is not None:
             self.weights_t = [torch.empty(w.dims[l + 1], w.dims[l], dtype=self.act, device=dev) for l in range(L)]
+        # layout of the forward MatMul ("NN": H W; "NT": H (W^T)^T)
+        self.forward_layout = "NT" if self.weights_t is not None else "NN"
         self.target = None if inputs["target"] is None else _to_device(inputs["target"], w.act, dev)
         self.upstream = None if inputs["upstream"] is None else _to_device(inputs["upstream"], w.act, dev)
 

@@ -19,7 +19,8 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtfdense.so")
+# TFD_LIBRARY points at another build of the same library (tuning variants).
+LIB_PATH = os.environ.get("TFD_LIBRARY") or os.path.join(_HERE, "libtfdense.so")
 
 TFD_OK, TFD_EINVAL, TFD_EUNSUPPORTED, TFD_EHIP = 0, 1, 2, 3
 TFD_F32, TFD_BF16 = 0, 1

@@ -128,6 +128,17 @@ def test_matmul_bf16_whole_tiles(m, n, k, layout, dout, epi):
         assert bad == 0
 
 
+@pytest.mark.parametrize("waves", [4, 8, 16])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_matmul_bf16_every_wave_layout(layout, waves, monkeypatch):
+    """Every workgroup shape of the whole-tile kernel (the tuning override)."""
+    monkeypatch.setenv("TFD_BF16_WAVES", f"NN:{waves},NT:{waves},TN:{waves}")
+    got, want, _, D = _run_gemm(512, 768, 320, layout, "bf16", "bf16", "bias", seed=waves)
+    assert_close(got, want, D, TAU["bf16"], f"{layout} waves {waves}")
+    got, want, _, _ = _run_gemm(512, 256, 128, layout, "bf16", "f32", "none", kind="int")
+    assert_bits(got, want, f"integer {layout} waves {waves}")
+
+
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 def test_matmul_bf16_whole_tiles_integers_exact(layout):
     got, want, _, _ = _run_gemm(512, 512, 64, layout, "bf16", "bf16", "none", kind="int")
