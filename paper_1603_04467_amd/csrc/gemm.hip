@@ -322,9 +322,11 @@ hipError_t launch_cfg(const GemmDesc& d, hipStream_t s) {
 }
 
 // Tile configuration: 0 = pick by problem size (16-bit operands on whole
-// 256 x 256 tiles go to the direct-to-LDS kernel of gemm_bf16.hip), 1 = 256x256 (4 waves of
-// 128x128), 2 = 256x128 (4 waves of 128x64), 3 = 128x128 (4 waves of 64x64),
-// 4 = 64x64 (4 waves of 32x32). Non-zero values come from the tuning-only
+// 256 x 256 tiles go to the direct-to-LDS kernel of gemm_bf16.hip),
+// 1 = 256x256 (4 waves of 128x128), 2 = 256x128 (4 waves of 128x64),
+// 3 = 128x128 (4 waves of 64x64), 4 = 64x64 (4 waves of 32x32); fp32 only:
+// 5 = 256x256 (8 waves of 128x64), 6 = 256x256 (16 waves of 64x64),
+// 7 = 128x128 (8 waves of 64x32). Non-zero values come from the tuning-only
 // environment variable TFD_GEMM_TILE.
 template <typename T, typename OutT, bool TA, bool TB>
 hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t s) {
@@ -332,7 +334,16 @@ hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t 
   if (tile == 0) {
     const int64_t tiles256 = ((d.m + 255) / 256) * ((d.n + 255) / 256);
     const int64_t tiles128 = ((d.m + 127) / 128) * ((d.n + 127) / 128);
-    tile = tiles256 >= 128 ? 1 : (tiles128 >= 128 ? 3 : 4);
+    // fp32: 256x256 with 8 waves (2 per SIMD) measured fastest inside the step
+    tile = tiles256 >= 128 ? (sizeof(T) == 4 ? 5 : 1) : (tiles128 >= 128 ? 3 : 4);
+  }
+  if constexpr (sizeof(T) == 4) {  // fp32-only shapes
+    switch (tile) {
+      case 5: return launch_cfg<T, OutT, TA, TB, 256, 256, 2, 4, true>(d, s);
+      case 6: return launch_cfg<T, OutT, TA, TB, 256, 256, 4, 4, true>(d, s);
+      case 7: return launch_cfg<T, OutT, TA, TB, 128, 128, 2, 4, true>(d, s);
+      default: break;
+    }
   }
   switch (tile) {
     case 1: return launch_cfg<T, OutT, TA, TB, 256, 256, 2, 2, true>(d, s);
