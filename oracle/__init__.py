@@ -34,6 +34,8 @@ from .dense import (  # noqa: F401
     relu_grad,
     bias_add_grad,
     l2_loss_grad,
+    softmax,
+    softmax_cross_entropy_grad,
     apply_gradient_descent,
     dense_step,
 )

@@ -164,6 +164,35 @@ def l2_loss_grad(output, target=None, grad_dtype="f32"):
     return round_to(d, grad_dtype), loss
 
 
+def softmax(logits):
+    """SoftMax of section 2, Table 1, over the last axis:
+    ``p[n, c] = exp(z[n, c]) / sum_j exp(z[n, j])``, evaluated with the row
+    maximum subtracted (the same value, without overflow)."""
+    z = np.asarray(logits, dtype=np.float64)
+    e = np.exp(z - z.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def softmax_cross_entropy_grad(logits, labels, grad_dtype="f32"):
+    """Classifier cost on the output layer: ``L = -sum_n log softmax(z_n)[y_n]``
+    (a sum over the batch, like the squared error) and its gradient with
+    respect to the logits, ``G = softmax(z) - onehot(y)``.
+
+    Figure 1 leaves the cost open; this one is built from the SoftMax and Log
+    ops of Table 1. ``L`` uses ``log sum_j exp(z_j) - z_y`` in float64; ``G`` is
+    rounded once to ``grad_dtype``.
+    """
+    z = np.asarray(logits, dtype=np.float64)
+    y = np.asarray(labels, dtype=np.int64)
+    n = z.shape[0]
+    m = z.max(axis=1)
+    lse = m + np.log(np.exp(z - m[:, None]).sum(axis=1))
+    loss = float(np.sum(lse - z[np.arange(n), y]))
+    g = softmax(z)
+    g[np.arange(n), y] -= 1.0
+    return round_to(g, grad_dtype), loss
+
+
 # --------------------------------------------------------------------------
 # Stateful update (section 2 "Variables"; SGD of section 4.1)
 # --------------------------------------------------------------------------
@@ -214,14 +243,15 @@ def apply_gradient_descent(var, alpha, delta, dtype="f32"):
 # --------------------------------------------------------------------------
 
 def dense_step(x, weights, biases, relus, act="f32", target=None, upstream_grad=None,
-               lr=0.01, masters=None, update=True):
+               lr=0.01, masters=None, update=True, labels=None):
     """Forward, gradient subgraph and SGD update of ``len(weights)`` dense
     layers, in the order a dependency-respecting schedule runs them.
 
     Forward (Figure 1): ``H_l = Relu(H_{l-1} @ W_l + b_l)`` (identity where
     ``relus[l]`` is False), stored in ``act``.
     Cost (section 4.1 computes ``dC/dX`` for a cost C): ``l2_loss_grad`` of
-    the last output against ``target``, or the given ``upstream_grad``.
+    the last output against ``target``, ``softmax_cross_entropy_grad`` against
+    class ``labels``, or the given ``upstream_grad``.
     Backward, last layer first (section 4.1 backtracks from C): the ReLU
     gradient ``dY_l = relu_grad(G_l, H_l)`` (``dY_l = G_l`` on an identity
     layer), ``db_l = bias_add_grad(dY_l)``, ``dX_l = dY_l @ W_l.T`` (stored in
@@ -244,6 +274,8 @@ def dense_step(x, weights, biases, relus, act="f32", target=None, upstream_grad=
 
     if upstream_grad is not None:
         g, loss = np.asarray(upstream_grad, dtype=np.float64), None
+    elif labels is not None:
+        g, loss = softmax_cross_entropy_grad(h[L], labels, grad_dtype=act)
     else:
         g, loss = l2_loss_grad(h[L], target, grad_dtype=act)
     top_grad = g
