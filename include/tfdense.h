@@ -164,6 +164,28 @@ TFD_API tfd_status tfd_l2_loss_grad(const void* output, const void* target, void
                             int64_t count, tfd_dtype type,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/* Workspace bytes that tfd_softmax_cross_entropy_grad needs for `rows` rows. */
+TFD_API size_t tfd_softmax_xent_workspace_size(int64_t rows);
+
+/*
+ * Classifier cost head: SoftMax (section 2, Table 1) of each row of
+ * logits[rows x cols] (row-major, contiguous), its cross-entropy against one
+ * integer class label per row, and the gradient with respect to the logits:
+ *   p[r, :]    = softmax(logits[r, :]),
+ *   loss       = sum_r ( log sum_c exp(logits[r, c]) - logits[r, labels[r]] ),
+ *   grad[r, c] = p[r, c] - (c == labels[r])   (rounded once to `type`).
+ * labels is a device int32[rows]. Work is fp32 with the row maximum
+ * subtracted before exp; each row's loss term is formed in float64 from the
+ * fp32 log-sum-exp and summed in a fixed order, so `loss` (a device double)
+ * is reproducible bit for bit. A label outside [0, cols) is not detected on
+ * the host: that row's gradient is p with nothing subtracted and its loss
+ * term, hence `loss`, is NaN. rows = 0 writes loss = 0; cols must be >= 1
+ * when rows > 0. grad must not overlap logits, labels, loss or workspace.
+ */
+TFD_API tfd_status tfd_softmax_cross_entropy_grad(const void* logits, const int32_t* labels, void* grad,
+                                          double* loss, int64_t rows, int64_t cols, tfd_dtype type,
+                                          void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * ApplyGradientDescent on an fp32 Variable (section 2 "Variables"; the SGD
  * step of section 4.1), in place:

@@ -219,6 +219,38 @@ tfd_status tfd_l2_loss_grad(const void* output, const void* target, void* grad, 
                     "tfd_l2_loss_grad launch");
 }
 
+size_t tfd_softmax_xent_workspace_size(int64_t rows) {
+  if (rows < 0) return 0;
+  return tfd::softmax_xent_ws_bytes(rows);
+}
+
+tfd_status tfd_softmax_cross_entropy_grad(const void* logits, const int32_t* labels, void* grad, double* loss,
+                                          int64_t rows, int64_t cols, tfd_dtype type, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: negative size");
+  if (rows > 0 && cols == 0) return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: rows > 0 with cols = 0");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: unknown element type");
+  if (!loss) return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: loss is NULL");
+  if (rows > 0 && (!logits || !labels || !grad))
+    return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: NULL pointer");
+  if (rows > (int64_t)INT32_MAX * 4 || cols > (int64_t)INT32_MAX)
+    return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: size out of range");
+  const size_t need = tfd::softmax_xent_ws_bytes(rows);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: workspace of %zu bytes needed, %zu given", need,
+                workspace_bytes);
+  const size_t bytes = (size_t)rows * (size_t)cols * elem_bytes(type);
+  const size_t lbytes = (size_t)rows * sizeof(int32_t);
+  if (overlaps(grad, bytes, logits, bytes) || overlaps(grad, bytes, labels, lbytes) || overlaps(grad, bytes, loss, 8) ||
+      overlaps(grad, bytes, workspace, need) || overlaps(loss, 8, workspace, need) ||
+      overlaps(loss, 8, labels, lbytes) || overlaps(loss, 8, logits, bytes))
+    return fail(TFD_EINVAL, "tfd_softmax_cross_entropy_grad: overlapping buffers");
+  return hip_status(tfd::launch_softmax_xent(logits, labels, grad, loss, rows, cols, type == TFD_BF16, workspace,
+                                             as_stream(stream)),
+                    "tfd_softmax_cross_entropy_grad launch");
+}
+
 tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delta, int64_t count,
                                       uint16_t* var_bf16, void* stream) {
   g_err[0] = 0;

@@ -46,6 +46,10 @@ size_t loss_ws_bytes(int64_t count, bool bf16);
 hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, double* loss,
                                int64_t count, bool bf16, void* ws, hipStream_t s);
 
+size_t softmax_xent_ws_bytes(int64_t rows);
+hipError_t launch_softmax_xent(const void* logits, const int32_t* labels, void* grad, double* loss, int64_t rows,
+                               int64_t cols, bool bf16, void* ws, hipStream_t s);
+
 hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow,
                       hipStream_t s);
 hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,

@@ -6,7 +6,9 @@ would take (section 3.1 runs a node once its inputs are ready; section 2's
 control dependencies order a Variable's readers before its writer):
 
   forward  l = 1..L : H_l = Relu(H_{l-1} W_l + b_l)   (identity on the output layer)
-  cost              : G = H_L - T, L = 1/2 |G|^2     (or a given upstream gradient)
+  cost              : G = H_L - T, L = 1/2 |G|^2     (squared error), or
+                      G = softmax(H_L) - onehot(y), L = cross-entropy (class labels y),
+                      or a given upstream gradient
   backward l = L..1 : dY_l, db_l = ReluGrad + BiasAddGrad(G_l, H_l)
                       G_{l-1} = dX_l = dY_l W_l^T          (reads the old W_l)
                       dW_l = H_{l-1}^T dY_l
@@ -57,6 +59,8 @@ class DenseStep:
         self.forward_layout = "NT" if self.weights_t is not None else "NN"
         self.target = None if inputs["target"] is None else _to_device(inputs["target"], w.act, dev)
         self.upstream = None if inputs["upstream"] is None else _to_device(inputs["upstream"], w.act, dev)
+        labels = inputs.get("labels")
+        self.labels = None if labels is None else torch.from_numpy(np.ascontiguousarray(labels, np.int32)).to(dev)
 
         self.h = [self.x] + [torch.empty(N, w.dims[l + 1], dtype=self.act, device=dev) for l in range(L)]
         self.g = self.upstream if self.upstream is not None else torch.empty(N, w.dims[-1], dtype=self.act, device=dev)
@@ -69,6 +73,7 @@ class DenseStep:
 
         need = [T.tfd_reduction_workspace_size(N, w.dims[l + 1], self.act) for l in range(L)]
         need.append(T.tfd_loss_workspace_size(N * w.dims[-1], self.act))
+        need.append(T.tfd_softmax_xent_workspace_size(N))
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
         if self.weights_t is not None:
@@ -111,7 +116,10 @@ class DenseStep:
         if self.upstream is None:
             if mark:
                 mark("loss")
-            T.tfd_l2_loss_grad(self.h[L], self.target, self.g, self.loss, workspace=ws)
+            if self.labels is not None:
+                T.tfd_softmax_cross_entropy_grad(self.h[L], self.labels, self.g, self.loss, workspace=ws)
+            else:
+                T.tfd_l2_loss_grad(self.h[L], self.target, self.g, self.loss, workspace=ws)
         grad = self.g
         for l in reversed(range(L)):
             if mark:

@@ -30,7 +30,7 @@ EXPORTS = (
     "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
     "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
     "tfd_relu_grad_bias_add_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
-    "tfd_apply_gradient_descent", "tfd_apply_gradient_descent_matrix",
+    "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent", "tfd_apply_gradient_descent_matrix",
 )
 
 
@@ -66,6 +66,8 @@ def load() -> ctypes.CDLL:
         "tfd_relu_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
         "tfd_loss_workspace_size": ([i64, i32], sz),
         "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
+        "tfd_softmax_xent_workspace_size": ([i64], sz),
+        "tfd_softmax_cross_entropy_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
         "tfd_apply_gradient_descent": ([vp, ctypes.c_float, vp, i64, vp, vp], i32),
         "tfd_apply_gradient_descent_matrix": ([vp, ctypes.c_float, vp, i64, i64, vp, vp, vp], i32),
     }
@@ -196,6 +198,29 @@ def tfd_l2_loss_grad(output, target, grad, loss, workspace=None, stream=None):
     ws = _workspace(need, output.device, workspace)
     _check(load().tfd_l2_loss_grad(_ptr(output), _ptr(target), _ptr(grad), _ptr(loss), n, _dtype(output),
                                    _ptr(ws), ws.numel(), _stream(stream)))
+    return grad, loss
+
+
+def tfd_softmax_xent_workspace_size(rows) -> int:
+    return load().tfd_softmax_xent_workspace_size(rows)
+
+
+def tfd_softmax_cross_entropy_grad(logits, labels, grad, loss, workspace=None, stream=None):
+    """grad = softmax(logits) - onehot(labels), loss = summed cross-entropy
+    (a float64 device scalar); logits and grad are [rows, cols] contiguous,
+    labels int32[rows]."""
+    if logits.dim() != 2 or not logits.is_contiguous():
+        raise ValueError("logits must be a contiguous matrix")
+    rows, cols = logits.shape
+    if grad.shape != logits.shape or grad.dtype != logits.dtype or not grad.is_contiguous():
+        raise ValueError("grad must match logits")
+    if labels.dtype != torch.int32 or labels.numel() != rows or not labels.is_contiguous():
+        raise ValueError("labels must be contiguous int32 with one entry per row")
+    if loss.dtype != torch.float64 or loss.numel() < 1:
+        raise ValueError("loss must be a float64 tensor")
+    ws = _workspace(tfd_softmax_xent_workspace_size(rows), logits.device, workspace)
+    _check(load().tfd_softmax_cross_entropy_grad(_ptr(logits), _ptr(labels), _ptr(grad), _ptr(loss), rows, cols,
+                                                 _dtype(logits), _ptr(ws), ws.numel(), _stream(stream)))
     return grad, loss
 
 

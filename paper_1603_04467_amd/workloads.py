@@ -32,7 +32,8 @@ class Workload:
     ``weight_init``: ("normal", std) or ("glorot",).
     ``bias_init``: ("zero",) or ("normal", std).
     ``cost``: "half_sq" (1/2 sum h^2), "sq_err" (1/2 sum (h - t)^2 against
-    t ~ N(0,1)) or "upstream" (a given upstream gradient ~ N(0,1)).
+    t ~ N(0,1)), "xent" (softmax cross-entropy against class labels drawn
+    uniformly from [0, d_L)) or "upstream" (a given upstream gradient ~ N(0,1)).
     ``masters``: the updated fp32 Variables are separate from the 16-bit
     GEMM operands.
     """
@@ -82,6 +83,10 @@ WORKLOADS = {
         name="mlp784-1024-1024-10", wid=1, batch=256, dims=(784, 1024, 1024, 10),
         relus=(True, True, False), act="f32", input_dist="uniform01", weight_init=("glorot",),
         bias_init=("zero",), cost="sq_err"),
+    "mlp784-1024-1024-10-xent": Workload(
+        name="mlp784-1024-1024-10-xent", wid=5, batch=256, dims=(784, 1024, 1024, 10),
+        relus=(True, True, False), act="f32", input_dist="uniform01", weight_init=("glorot",),
+        bias_init=("zero",), cost="xent"),
     "wide4096x4-f32": Workload(
         name="wide4096x4-f32", wid=2, batch=8192, dims=(4096,) * 5, relus=(True, True, True, False),
         act="f32", input_dist="normal", weight_init=("normal", 1.0 / 64.0), bias_init=("zero",),
@@ -129,7 +134,7 @@ def generate(w: Workload, seed: int = 0) -> dict:
     Returns numpy arrays: float32 for fp32 tensors, uint16 bit patterns for
     16-bit tensors. Keys: ``x``, ``weights`` (GEMM operands), ``masters``
     (fp32 Variables, or None), ``biases`` (fp32), ``target`` or ``upstream``
-    (or None), plus ``act``.
+    (or None), ``labels`` (int32 class per row, or None), plus ``act``.
     """
     tid = 0
     out = {"act": w.act}
@@ -159,7 +164,10 @@ def generate(w: Workload, seed: int = 0) -> dict:
         target = _draw(_rng(seed, w.wid, tid), (w.batch, w.dims[-1]), ("normal", 1.0))
     elif w.cost == "upstream":
         upstream = _draw(_rng(seed, w.wid, tid), (w.batch, w.dims[-1]), ("normal", 1.0))
+    elif w.cost == "xent":
+        out["labels"] = _rng(seed, w.wid, tid).integers(0, w.dims[-1], size=w.batch, dtype=np.int32)
     tid += 1
+    out.setdefault("labels", None)
 
     if w.act == "bf16":
         out["x"] = to_bf16_bits(x)

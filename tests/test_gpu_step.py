@@ -39,6 +39,7 @@ def _host_inputs(w, inp):
         "biases": [a.astype(np.float64) for a in inp["biases"]],
         "target": None if inp["target"] is None else conv(inp["target"]),
         "upstream": None if inp["upstream"] is None else conv(inp["upstream"]),
+        "labels": inp.get("labels"),
     }
 
 
@@ -100,7 +101,7 @@ def _compare_full(w, inp, s):
     L = w.layers
     ref = oracle.dense_step(hi["x"], hi["weights"], hi["biases"], list(w.relus), act=w.act,
                             target=hi["target"], upstream_grad=hi["upstream"], lr=w.lr,
-                            masters=hi["masters"], update=w.update)
+                            masters=hi["masters"], update=w.update, labels=hi["labels"])
     h_gpu = [to_f64(t) for t in s.h]
     # forward
     D_fwd = []
@@ -121,7 +122,16 @@ def _compare_full(w, inp, s):
         touched_at[l] = touched.copy()
     # cost
     g_gpu = to_f64(s.g)
-    if ref["loss"] is not None:
+    if ref["loss"] is not None and hi["labels"] is not None:
+        # softmax is 1/2-Lipschitz per element in the max-norm of the logits,
+        # each row's cross-entropy 2-Lipschitz; the fp32 exp/log/sum add
+        # a few ulp of p and of log-sum-exp per row
+        D_G = D_fwd[-1] + amax(ref["g"])
+        assert_close(g_gpu, ref["g"], D_G, tau, "G")
+        C = w.dims[-1]
+        per_row = 2.0 * tau * D_fwd[-1] + (C / 64 + 80 + 2 * amax(ref["h"][L])) * 2.0 ** -23
+        _assert_within(np.array([s.loss.item()]), np.array([ref["loss"]]), w.batch * per_row, "loss")
+    elif ref["loss"] is not None:
         D_G = D_fwd[-1] + amax(ref["g"])
         assert_close(g_gpu, ref["g"], D_G, tau, "G")
         allowed = tau * D_fwd[-1] * float(np.sum(np.abs(ref["g"]))) + 1e-12 * ref["loss"]
@@ -169,6 +179,8 @@ def _compare_full(w, inp, s):
 SCALED = [
     ("dense784x100", None, None),
     ("mlp784-1024-1024-10", None, None),
+    ("mlp784-1024-1024-10-xent", None, None),
+    ("mlp784-1024-1024-10-xent", 200, (784, 1024, 1024, 1000)),
     ("wide4096x4-f32", 600, (256, 384, 264, 128, 200)),
     ("wide4096x4-f32", 520, (136, 256, 512, 264, 128)),
     ("wide4096x4-bf16", 600, (256, 384, 264, 128, 200)),
@@ -190,10 +202,10 @@ def test_step_matches_oracle(name, batch, dims):
     print(f"{w.name}: {flips} rows with in-band Relu mask differences")
 
 
-@pytest.mark.parametrize("name", ["dense784x100", "wide4096x4-bf16"])
+@pytest.mark.parametrize("name", ["dense784x100", "mlp784-1024-1024-10-xent", "wide4096x4-bf16"])
 def test_step_is_deterministic(name):
     w = workloads.workload(name)
-    if name != "dense784x100":
+    if name == "wide4096x4-bf16":
         w = w.scaled(batch=1032, dims=(512, 768, 512, 256, 512))
     inp = workloads.generate(w, seed=3)
     s = DenseStep(w, inp)
