@@ -39,7 +39,8 @@ HBM_PEAK_GBS = 8000.0
 PRIMARY = "wide4096x4-bf16"
 # timed in the same run and reported under "also": the fp32 twin, then the
 # MNIST-shaped steps (classifier head and squared-error head) and the single layer
-SECONDARY = ("wide4096x4-f32", "mlp784-1024-1024-10-xent", "mlp784-1024-1024-10", "dense784x100")
+SECONDARY = ("wide4096x4-f32", "wide4096x4-bf16-trunc", "mlp784-1024-1024-10-xent", "mlp784-1024-1024-10",
+             "dense784x100")
 
 
 def _gemm_bytes(shape, layout, eb):
@@ -240,6 +241,39 @@ def cpu_baseline(name: str, rows: int):
     }
 
 
+def time_conversions(count: int = 1 << 26, reps: int = 20):
+    """The 32 <-> 16-bit conversion ops of section 5.5 on `count` elements
+    (fp32 -> 16 truncating and nearest even, 16 -> fp32), resident in HBM:
+    mean launch time from HIP events and GB/s of compulsory traffic."""
+    import torch
+
+    from paper_1603_04467_amd import tfdense as T
+
+    stream = torch.cuda.current_stream()
+    src = torch.randn(count, device="cuda")
+    h = torch.empty(count, dtype=torch.bfloat16, device="cuda")
+    back = torch.empty(count, device="cuda")
+    calls = {
+        "f32_to_bf16_truncate": (lambda: T.tfd_convert_f32_to_bf16(src, h, rounding="truncate"), 6 * count),
+        "f32_to_bf16_nearest": (lambda: T.tfd_convert_f32_to_bf16(src, h, rounding="nearest"), 6 * count),
+        "bf16_to_f32": (lambda: T.tfd_convert_bf16_to_f32(h, back), 6 * count),
+    }
+    out = {}
+    for name, (fn, byt) in calls.items():
+        for _ in range(3):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for i in range(reps):
+            fn()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
+        out[name] = {"elements": count, "ms": round(ms, 4), "gbs": round(byt / (ms * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(byt / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3)}
+    return out
+
+
 def _per_op(ops):
     """Mean ms per op, with TFLOP/s (GEMMs) or GB/s (memory-bound ops)."""
     out = {}
@@ -321,6 +355,9 @@ def main():
                 "per_op": _per_op(r2["ops"]),
                 "loss": r2["loss"],
             })
+    if not args.no_secondary and args.workload == PRIMARY:
+        print("bench: timing the 32 <-> 16-bit conversions", file=sys.stderr, flush=True)
+        out["conversions"] = time_conversions()
     if not args.no_cpu_baseline:
         print(f"bench: timing the oracle on {args.cpu_rows} rows", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows)

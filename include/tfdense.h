@@ -15,7 +15,9 @@
  *  - Element types: TFD_F32 (IEEE binary32) and TFD_BF16 (the 16-bit float
  *    of section 5.5: binary32 with 16 fewer mantissa bits). Products are
  *    accumulated in fp32. Values stored as TFD_BF16 are rounded to nearest
- *    even. Biases, bias gradients and Variables are always fp32.
+ *    even, unless a call's tfd_rounding argument or TFD_EPI_TRUNCATE_16
+ *    selects the truncating converter of section 5.5. Biases, bias
+ *    gradients and Variables are always fp32.
  *  - Pointers are device pointers unless stated otherwise. The caller owns
  *    every buffer; the library allocates no device memory, keeps no state
  *    between calls and never synchronises. Scratch memory is passed in as a
@@ -45,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TFD_ABI_VERSION 1
+#define TFD_ABI_VERSION 2
 
 #if defined(__GNUC__)
 #define TFD_API __attribute__((visibility("default")))
@@ -62,12 +64,24 @@ typedef enum tfd_status {
 
 typedef enum tfd_dtype { TFD_F32 = 0, TFD_BF16 = 1 } tfd_dtype;
 
+/* How an fp32 value becomes a 16-bit one.
+ * TFD_ROUND_NEAREST_EVEN: to the nearest 16-bit value, ties to even (the
+ *   default of every call).
+ * TFD_ROUND_TRUNCATE: the lossy converter of section 5.5: the low 16 bits of
+ *   the fp32 pattern are dropped (rounding toward zero; infinities and zeros
+ *   keep their sign). A NaN becomes the quiet NaN 0x7FC0 with its sign, so
+ *   that no NaN turns into an infinity. */
+typedef enum tfd_rounding { TFD_ROUND_NEAREST_EVEN = 0, TFD_ROUND_TRUNCATE = 1 } tfd_rounding;
+
 /* What the MatMul producer applies to the fp32 accumulator before the
  * single rounding to the output type. */
 typedef enum tfd_epilogue {
   TFD_EPI_NONE = 0,      /* C = op(A) op(B)                                 */
   TFD_EPI_BIAS = 1,      /* C = op(A) op(B) + 1 bias^T        (Add, Fig. 1) */
-  TFD_EPI_BIAS_RELU = 2  /* C = Relu(op(A) op(B) + 1 bias^T)  (Relu(Wx+b))  */
+  TFD_EPI_BIAS_RELU = 2, /* C = Relu(op(A) op(B) + 1 bias^T)  (Relu(Wx+b))  */
+  /* Flag, OR-ed with one of the above: a 16-bit C is written with the
+   * truncating converter (TFD_ROUND_TRUNCATE) instead of nearest even. */
+  TFD_EPI_TRUNCATE_16 = 16
 } tfd_epilogue;
 
 TFD_API int tfd_abi_version(void);
@@ -190,12 +204,13 @@ TFD_API tfd_status tfd_softmax_cross_entropy_grad(const void* logits, const int3
  * ApplyGradientDescent on an fp32 Variable (section 2 "Variables"; the SGD
  * step of section 4.1), in place:
  *   var[i] = fma(-alpha, delta[i], var[i])   (one rounding),
- * and, when var_bf16 != NULL, var_bf16[i] = the updated var[i] rounded to
- * nearest even in the 16-bit format (the operand copy of 16-bit GEMMs).
+ * and, when var_bf16 != NULL, var_bf16[i] = the updated var[i] converted to
+ * the 16-bit format with `rounding` (the operand copy of 16-bit GEMMs).
  * delta must not overlap var.
  */
 TFD_API tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delta,
-                                      int64_t count, uint16_t* var_bf16, void* stream);
+                                      int64_t count, uint16_t* var_bf16, tfd_rounding rounding,
+                                      void* stream);
 
 /*
  * ApplyGradientDescent on an fp32 weight matrix var[rows x cols] (row-major,
@@ -210,7 +225,22 @@ TFD_API tfd_status tfd_apply_gradient_descent(float* var, float alpha, const flo
  */
 TFD_API tfd_status tfd_apply_gradient_descent_matrix(float* var, float alpha, const float* delta,
                                              int64_t rows, int64_t cols, uint16_t* var_bf16,
-                                             uint16_t* var_bf16_t, void* stream);
+                                             uint16_t* var_bf16_t, tfd_rounding rounding,
+                                             void* stream);
+
+/*
+ * The conversion nodes of section 5.5 ("lossy compression" of the tensors a
+ * Send/Recv pair moves between devices): fp32 -> 16 bits on the sending side,
+ * 16 bits -> fp32 on the receiving side.
+ *   tfd_convert_f32_to_bf16: dst[i] = 16-bit pattern of src[i] under
+ *     `rounding` (TFD_ROUND_TRUNCATE is the paper's converter).
+ *   tfd_convert_bf16_to_f32: dst[i] = the fp32 whose high half is src[i] and
+ *     whose low 16 bits are zero (exact; NaN payloads are kept).
+ * Contiguous arrays of `count` elements; src and dst must not overlap.
+ */
+TFD_API tfd_status tfd_convert_f32_to_bf16(const float* src, uint16_t* dst, int64_t count,
+                                   tfd_rounding rounding, void* stream);
+TFD_API tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int64_t count, void* stream);
 
 #ifdef __cplusplus
 }

@@ -7,11 +7,14 @@ The product path never calls it, and it imports nothing from the product
 package (the two share no code; the seeded input generator hands both sides
 the same arrays).
 
-Every function works on float64 numpy arrays. Sums and dot products are
+Every function works on float64 numpy arrays. The 32 <-> 16-bit converter
+of section 5.5 lives in ``oracle.convert`` (a C loop compiled with gcc on
+first use). Sums and dot products are
 carried out in float64 from the stored values (bf16 and fp32 values upcast
 exactly) and rounded once, round-to-nearest-even, to the storage type at the
 points where a tensor is stored. Storage types are named ``"f64"`` (no
-rounding; used by the finite-difference pins), ``"f32"`` and ``"bf16"``.
+rounding; used by the finite-difference pins), ``"f32"``, ``"bf16"`` and
+``"bf16t"`` (fp32 first, then the truncating converter).
 
 Pins (see ``tests/test_oracle_*.py``): brute-force triple loops, identity and
 permutation matrices, exact small-integer sums, finite differences of the

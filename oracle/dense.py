@@ -17,7 +17,7 @@ from __future__ import annotations
 
 import numpy as np
 
-STORAGE_TYPES = ("f64", "f32", "bf16")
+STORAGE_TYPES = ("f64", "f32", "bf16", "bf16t")
 
 # Largest finite value of the 16-bit format: fp32's exponent range with an
 # 8-bit significand, (2 - 2**-7) * 2**127.
@@ -63,6 +63,11 @@ def round_to(x, dtype: str) -> np.ndarray:
         return x.astype(np.float32).astype(np.float64)
     if dtype == "bf16":
         return round_bf16(x)
+    if dtype == "bf16t":
+        # the 16-bit format reached through the lossy converter of section
+        # 5.5: the producer's fp32 value (one rounding), then truncation
+        from .convert import truncate_bf16
+        return truncate_bf16(x)
     raise ValueError(f"unknown storage type {dtype!r}")
 
 
@@ -243,7 +248,7 @@ def apply_gradient_descent(var, alpha, delta, dtype="f32"):
 # --------------------------------------------------------------------------
 
 def dense_step(x, weights, biases, relus, act="f32", target=None, upstream_grad=None,
-               lr=0.01, masters=None, update=True, labels=None):
+               lr=0.01, masters=None, update=True, labels=None, rounding="nearest"):
     """Forward, gradient subgraph and SGD update of ``len(weights)`` dense
     layers, in the order a dependency-respecting schedule runs them.
 
@@ -263,14 +268,21 @@ def dense_step(x, weights, biases, relus, act="f32", target=None, upstream_grad=
     weights themselves) are the fp32 Variables that are updated. With 16-bit
     activations the operand is re-derived from the updated master by
     rounding.
+    ``rounding="truncate"`` (16-bit activations only) stores the forward
+    outputs H, the input gradients dX and the re-derived 16-bit weights
+    through the truncating converter of section 5.5 instead of rounding to
+    nearest even; the cost gradient keeps its exact rounding.
     """
     L = len(weights)
     if not (len(biases) == len(relus) == L):
         raise ValueError("one bias and one activation flag per layer")
     var_t = "f64" if act == "f64" else "f32"
+    if rounding not in ("nearest", "truncate") or (rounding == "truncate" and act != "bf16"):
+        raise ValueError("truncation applies to 16-bit activations only")
+    store = "bf16t" if rounding == "truncate" else act
     h = [np.asarray(x, dtype=np.float64)]
     for l in range(L):
-        h.append(matmul(h[l], weights[l], out=act, bias=biases[l], relu=relus[l]))
+        h.append(matmul(h[l], weights[l], out=store, bias=biases[l], relu=relus[l]))
 
     if upstream_grad is not None:
         g, loss = np.asarray(upstream_grad, dtype=np.float64), None
@@ -290,14 +302,14 @@ def dense_step(x, weights, biases, relus, act="f32", target=None, upstream_grad=
     for l in reversed(range(L)):
         dy[l] = relu_grad(g, h[l + 1]) if relus[l] else g
         db[l] = bias_add_grad(dy[l], out=var_t)
-        dx[l] = matmul(dy[l], weights[l], transpose_b=True, out=act)
+        dx[l] = matmul(dy[l], weights[l], transpose_b=True, out=store)
         dw[l] = matmul(h[l], dy[l], transpose_a=True, out=var_t)
         if update:
             master = weights[l] if masters is None else masters[l]
             m_new = apply_gradient_descent(master, lr, dw[l], dtype=var_t)
             if masters is not None:
                 new_m[l] = m_new
-            new_w[l] = round_to(m_new, act) if act == "bf16" else m_new
+            new_w[l] = round_to(m_new, store) if act == "bf16" else m_new
             new_b[l] = apply_gradient_descent(biases[l], lr, db[l], dtype=var_t)
         g = dx[l]
 

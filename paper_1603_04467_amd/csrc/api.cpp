@@ -28,6 +28,7 @@ tfd_status hip_status(hipError_t e, const char* what) {
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 bool valid_dtype(tfd_dtype t) { return t == TFD_F32 || t == TFD_BF16; }
+bool valid_rounding(tfd_rounding r) { return r == TFD_ROUND_NEAREST_EVEN || r == TFD_ROUND_TRUNCATE; }
 int elem_bytes(tfd_dtype t) { return t == TFD_BF16 ? 2 : 4; }
 
 // Byte ranges [p, p + bytes) overlap?
@@ -70,8 +71,12 @@ tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, in
   if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "tfd_matmul: negative size m=%lld n=%lld k=%lld", (long long)m, (long long)n, (long long)k);
   if (!valid_dtype(a_type) || !valid_dtype(b_type) || !valid_dtype(c_type))
     return fail(TFD_EINVAL, "tfd_matmul: unknown element type");
-  if (epilogue != TFD_EPI_NONE && epilogue != TFD_EPI_BIAS && epilogue != TFD_EPI_BIAS_RELU)
+  const bool trunc16 = ((int)epilogue & TFD_EPI_TRUNCATE_16) != 0;
+  const int op = (int)epilogue & ~(int)TFD_EPI_TRUNCATE_16;
+  if (op != TFD_EPI_NONE && op != TFD_EPI_BIAS && op != TFD_EPI_BIAS_RELU)
     return fail(TFD_EINVAL, "tfd_matmul: unknown epilogue %d", (int)epilogue);
+  if (trunc16 && c_type != TFD_BF16)
+    return fail(TFD_EINVAL, "tfd_matmul: TFD_EPI_TRUNCATE_16 needs a 16-bit output");
   if (transpose_a && transpose_b)
     return fail(TFD_EUNSUPPORTED, "tfd_matmul: transpose_a and transpose_b together are not implemented");
   if (a_type != b_type || (a_type == TFD_F32 && c_type != TFD_F32))
@@ -86,12 +91,12 @@ tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, in
   if (m == 0 || n == 0) return TFD_OK;
   if (!c) return fail(TFD_EINVAL, "tfd_matmul: c is NULL");
   if (k > 0 && (!a || !b)) return fail(TFD_EINVAL, "tfd_matmul: a or b is NULL");
-  if (epilogue != TFD_EPI_NONE && !bias) return fail(TFD_EINVAL, "tfd_matmul: the bias epilogue needs a bias");
+  if (op != TFD_EPI_NONE && !bias) return fail(TFD_EINVAL, "tfd_matmul: the bias epilogue needs a bias");
   const int ab = elem_bytes(a_type), cb = elem_bytes(c_type);
   const size_t c_span = span(m, n, ldc, cb);
   if (overlaps(c, c_span, a, span(a_rows, a_cols, lda, ab)) ||
       overlaps(c, c_span, b, span(b_rows, b_cols, ldb, ab)) ||
-      (epilogue != TFD_EPI_NONE && overlaps(c, c_span, bias, (size_t)n * 4)))
+      (op != TFD_EPI_NONE && overlaps(c, c_span, bias, (size_t)n * 4)))
     return fail(TFD_EINVAL, "tfd_matmul: c overlaps an input");
   tfd::GemmDesc d;
   d.ta = transpose_a != 0;
@@ -108,7 +113,7 @@ tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, in
   d.in_bf16 = a_type == TFD_BF16;
   d.out_bf16 = c_type == TFD_BF16;
   d.bias = bias;
-  d.epi = (int)epilogue;
+  d.epi = op | (trunc16 ? tfd::kEpiTrunc16 : 0);
   return hip_status(tfd::launch_gemm(d, as_stream(stream)), "tfd_matmul launch");
 }
 
@@ -252,24 +257,27 @@ tfd_status tfd_softmax_cross_entropy_grad(const void* logits, const int32_t* lab
 }
 
 tfd_status tfd_apply_gradient_descent(float* var, float alpha, const float* delta, int64_t count,
-                                      uint16_t* var_bf16, void* stream) {
+                                      uint16_t* var_bf16, tfd_rounding rounding, void* stream) {
   g_err[0] = 0;
   if (count < 0) return fail(TFD_EINVAL, "tfd_apply_gradient_descent: negative count");
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "tfd_apply_gradient_descent: unknown rounding");
   if (count == 0) return TFD_OK;
   if (!var || !delta) return fail(TFD_EINVAL, "tfd_apply_gradient_descent: NULL pointer");
   const size_t bytes = (size_t)count * 4;
   if (overlaps(var, bytes, delta, bytes) || overlaps(var_bf16, (size_t)count * 2, var, bytes) ||
       overlaps(var_bf16, (size_t)count * 2, delta, bytes))
     return fail(TFD_EINVAL, "tfd_apply_gradient_descent: overlapping buffers");
-  return hip_status(tfd::launch_sgd(var, alpha, delta, count, var_bf16, as_stream(stream)),
+  return hip_status(tfd::launch_sgd(var, alpha, delta, count, var_bf16, rounding == TFD_ROUND_TRUNCATE,
+                                    as_stream(stream)),
                     "tfd_apply_gradient_descent launch");
 }
 
 tfd_status tfd_apply_gradient_descent_matrix(float* var, float alpha, const float* delta, int64_t rows,
                                              int64_t cols, uint16_t* var_bf16, uint16_t* var_bf16_t,
-                                             void* stream) {
+                                             tfd_rounding rounding, void* stream) {
   g_err[0] = 0;
   if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: negative size");
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: unknown rounding");
   if (rows == 0 || cols == 0) return TFD_OK;
   if (!var || !delta) return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: NULL pointer");
   const size_t n = (size_t)rows * (size_t)cols;
@@ -277,8 +285,32 @@ tfd_status tfd_apply_gradient_descent_matrix(float* var, float alpha, const floa
       overlaps(var_bf16, n * 2, delta, n * 4) || overlaps(var_bf16_t, n * 2, var, n * 4) ||
       overlaps(var_bf16_t, n * 2, delta, n * 4) || overlaps(var_bf16, n * 2, var_bf16_t, n * 2))
     return fail(TFD_EINVAL, "tfd_apply_gradient_descent_matrix: overlapping buffers");
-  return hip_status(tfd::launch_sgd_matrix(var, alpha, delta, rows, cols, var_bf16, var_bf16_t, as_stream(stream)),
+  return hip_status(tfd::launch_sgd_matrix(var, alpha, delta, rows, cols, var_bf16, var_bf16_t,
+                                           rounding == TFD_ROUND_TRUNCATE, as_stream(stream)),
                     "tfd_apply_gradient_descent_matrix launch");
+}
+
+tfd_status tfd_convert_f32_to_bf16(const float* src, uint16_t* dst, int64_t count, tfd_rounding rounding,
+                                   void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_convert_f32_to_bf16: negative count");
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "tfd_convert_f32_to_bf16: unknown rounding");
+  if (count == 0) return TFD_OK;
+  if (!src || !dst) return fail(TFD_EINVAL, "tfd_convert_f32_to_bf16: NULL pointer");
+  if (overlaps(src, (size_t)count * 4, dst, (size_t)count * 2))
+    return fail(TFD_EINVAL, "tfd_convert_f32_to_bf16: src and dst overlap");
+  return hip_status(tfd::launch_convert_to_bf16(src, dst, count, rounding == TFD_ROUND_TRUNCATE, as_stream(stream)),
+                    "tfd_convert_f32_to_bf16 launch");
+}
+
+tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int64_t count, void* stream) {
+  g_err[0] = 0;
+  if (count < 0) return fail(TFD_EINVAL, "tfd_convert_bf16_to_f32: negative count");
+  if (count == 0) return TFD_OK;
+  if (!src || !dst) return fail(TFD_EINVAL, "tfd_convert_bf16_to_f32: NULL pointer");
+  if (overlaps(src, (size_t)count * 2, dst, (size_t)count * 4))
+    return fail(TFD_EINVAL, "tfd_convert_bf16_to_f32: src and dst overlap");
+  return hip_status(tfd::launch_convert_to_f32(src, dst, count, as_stream(stream)), "tfd_convert_bf16_to_f32 launch");
 }
 
 }  // extern "C"

@@ -27,6 +27,18 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
   return __builtin_bit_cast(float, bits16 << 16);
 }
 
+// The lossy 32 -> 16-bit converter of section 5.5: the low 16 mantissa bits
+// are dropped (rounding toward zero). A NaN becomes the quiet NaN 0x7FC0 with
+// its sign kept, so that no NaN turns into an infinity.
+__device__ __forceinline__ uint16_t bf16_bits_trunc(float x) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, x);
+  return x != x ? (uint16_t)(0x7FC0u | ((u >> 16) & 0x8000u)) : (uint16_t)(u >> 16);
+}
+// 16-bit pattern of x under the selected conversion (truncating or nearest even).
+__device__ __forceinline__ uint16_t bf16_bits_mode(float x, bool trunc) {
+  return trunc ? bf16_bits_trunc(x) : bf16_bits(x);
+}
+
 // Relu as a bit select: y > 0 ? y : +0. Written on the bit pattern so the
 // compiler cannot turn it into a max, whose result for -0 is not +0.
 __device__ __forceinline__ float relu_f32(float y) {
@@ -47,5 +59,13 @@ __device__ __forceinline__ float load_f32(const float* p) { return *p; }
 __device__ __forceinline__ float load_f32(const bf16* p) { return to_f32(*p); }
 __device__ __forceinline__ void store_from_f32(float* p, float v) { *p = v; }
 __device__ __forceinline__ void store_from_f32(bf16* p, float v) { *p = to_bf16(v); }
+// Same, with the 16-bit conversion selectable (ignored for fp32 outputs).
+__device__ __forceinline__ void store_from_f32(float* p, float v, bool) { *p = v; }
+__device__ __forceinline__ void store_from_f32(bf16* p, float v, bool trunc) {
+  if (trunc)
+    *reinterpret_cast<uint16_t*>(p) = bf16_bits_trunc(v);
+  else
+    *p = to_bf16(v);
+}
 
 }  // namespace tfd

@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kThreads) void loss_final_kernel(const double* part
 // ---------------------------------------------------------------- ApplyGradientDescent
 template <bool VEC, bool SHADOW>
 __global__ __launch_bounds__(kThreads) void sgd_kernel(float* var, float alpha, const float* delta,
-                                                       int64_t count, uint16_t* shadow) {
+                                                       int64_t count, uint16_t* shadow, bool trunc) {
   const int64_t chunk = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const float na = -alpha;
   if (VEC) {
@@ -213,22 +213,22 @@ __global__ __launch_bounds__(kThreads) void sgd_kernel(float* var, float alpha, 
       for (int e = 0; e < 4; ++e) v[e] = __builtin_fmaf(na, d[e], v[e]);
       *reinterpret_cast<f32x4*>(var + i0) = v;
       if (SHADOW) {
-        const uint32_t lo = (uint32_t)bf16_bits(v[0]) | ((uint32_t)bf16_bits(v[1]) << 16);
-        const uint32_t hi = (uint32_t)bf16_bits(v[2]) | ((uint32_t)bf16_bits(v[3]) << 16);
+        const uint32_t lo = (uint32_t)bf16_bits_mode(v[0], trunc) | ((uint32_t)bf16_bits_mode(v[1], trunc) << 16);
+        const uint32_t hi = (uint32_t)bf16_bits_mode(v[2], trunc) | ((uint32_t)bf16_bits_mode(v[3], trunc) << 16);
         *reinterpret_cast<uint2*>(shadow + i0) = make_uint2(lo, hi);
       }
     } else {
       for (int64_t i = i0; i < count; ++i) {
         const float v = __builtin_fmaf(na, delta[i], var[i]);
         var[i] = v;
-        if (SHADOW) shadow[i] = bf16_bits(v);
+        if (SHADOW) shadow[i] = bf16_bits_mode(v, trunc);
       }
     }
   } else {
     if (chunk < count) {
       const float v = __builtin_fmaf(na, delta[chunk], var[chunk]);
       var[chunk] = v;
-      if (SHADOW) shadow[chunk] = bf16_bits(v);
+      if (SHADOW) shadow[chunk] = bf16_bits_mode(v, trunc);
     }
   }
 }
@@ -243,7 +243,7 @@ template <bool VEC>
 __global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict__ var, float alpha,
                                                               const float* __restrict__ delta, int64_t rows,
                                                               int64_t cols, uint16_t* __restrict__ shadow,
-                                                              uint16_t* __restrict__ shadow_t) {
+                                                              uint16_t* __restrict__ shadow_t, bool trunc) {
   __shared__ uint16_t tile[kSgdTile][kSgdTile + 2];
   const int64_t r0 = (int64_t)blockIdx.y * kSgdTile, c0 = (int64_t)blockIdx.x * kSgdTile;
   const int tid = threadIdx.x;
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict_
       uint16_t b[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        b[e] = bf16_bits(v[e]);
+        b[e] = bf16_bits_mode(v[e], trunc);
         tile[rr][cc + e] = b[e];
       }
       if (shadow)
@@ -278,7 +278,7 @@ __global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict_
         const int64_t off = r * cols + c;
         const float v = __builtin_fmaf(na, delta[off], var[off]);
         var[off] = v;
-        const uint16_t b = bf16_bits(v);
+        const uint16_t b = bf16_bits_mode(v, trunc);
         tile[rr][cc] = b;
         if (shadow) shadow[off] = b;
       }
@@ -308,14 +308,16 @@ __global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict_
 }  // namespace
 
 hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,
-                             uint16_t* shadow, uint16_t* shadow_t, hipStream_t s) {
+                             uint16_t* shadow, uint16_t* shadow_t, bool trunc, hipStream_t s) {
   const bool vec = aligned16(var) && aligned16(delta) && cols % 4 == 0 &&
                    ((reinterpret_cast<uintptr_t>(shadow) & 7) == 0) && aligned16(shadow_t);
   dim3 grid((unsigned)((cols + kSgdTile - 1) / kSgdTile), (unsigned)((rows + kSgdTile - 1) / kSgdTile));
   if (vec)
-    hipLaunchKernelGGL((sgd_matrix_kernel<true>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow, shadow_t);
+    hipLaunchKernelGGL((sgd_matrix_kernel<true>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow, shadow_t,
+                       trunc);
   else
-    hipLaunchKernelGGL((sgd_matrix_kernel<false>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow, shadow_t);
+    hipLaunchKernelGGL((sgd_matrix_kernel<false>), grid, kThreads, 0, s, var, alpha, delta, rows, cols, shadow,
+                       shadow_t, trunc);
   return hipGetLastError();
 }
 
@@ -391,16 +393,16 @@ hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, 
   return hipGetLastError();
 }
 
-hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow,
+hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow, bool trunc,
                       hipStream_t s) {
   const bool vec = aligned16(var) && aligned16(delta) && ((reinterpret_cast<uintptr_t>(shadow) & 7) == 0);
   const unsigned g = grid_for(vec ? (count + 3) / 4 : count);
   if (vec) {
-    if (shadow) hipLaunchKernelGGL((sgd_kernel<true, true>), g, kThreads, 0, s, var, alpha, delta, count, shadow);
-    else hipLaunchKernelGGL((sgd_kernel<true, false>), g, kThreads, 0, s, var, alpha, delta, count, shadow);
+    if (shadow) hipLaunchKernelGGL((sgd_kernel<true, true>), g, kThreads, 0, s, var, alpha, delta, count, shadow, trunc);
+    else hipLaunchKernelGGL((sgd_kernel<true, false>), g, kThreads, 0, s, var, alpha, delta, count, shadow, trunc);
   } else {
-    if (shadow) hipLaunchKernelGGL((sgd_kernel<false, true>), g, kThreads, 0, s, var, alpha, delta, count, shadow);
-    else hipLaunchKernelGGL((sgd_kernel<false, false>), g, kThreads, 0, s, var, alpha, delta, count, shadow);
+    if (shadow) hipLaunchKernelGGL((sgd_kernel<false, true>), g, kThreads, 0, s, var, alpha, delta, count, shadow, trunc);
+    else hipLaunchKernelGGL((sgd_kernel<false, false>), g, kThreads, 0, s, var, alpha, delta, count, shadow, trunc);
   }
   return hipGetLastError();
 }

@@ -280,11 +280,12 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
 
   // Epilogue: bias, Relu, one rounding to OutT.
   OutT* C = static_cast<OutT*>(p.c);
+  const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
 #pragma unroll
   for (int j = 0; j < FN; ++j) {
     const int col = n0 + wave_n * WTN + j * 32 + l32;
     const bool col_ok = col < p.n;
-    const float bv = (p.epi != 0 && col_ok) ? p.bias[col] : 0.0f;
+    const float bv = ((p.epi & kEpiOpMask) != 0 && col_ok) ? p.bias[col] : 0.0f;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -292,8 +293,8 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
         const int row = m0 + wave_m * WTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         if (col_ok && row < p.m) {
           float v = acc[i][j][r] + bv;
-          if (p.epi == 2) v = relu_f32(v);
-          store_from_f32(C + (int64_t)row * p.ldc + col, v);
+          if ((p.epi & kEpiOpMask) == 2) v = relu_f32(v);
+          store_from_f32(C + (int64_t)row * p.ldc + col, v, trunc16);
         }
       }
     }

@@ -205,18 +205,19 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   }
 
   OutT* C = static_cast<OutT*>(p.c);
+  const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
 #pragma unroll
   for (int j = 0; j < kFN; ++j) {
     const int col = n0 + wn * kWTN + j * 32 + l32;
-    const float bv = p.epi != 0 ? p.bias[col] : 0.0f;
+    const float bv = (p.epi & kEpiOpMask) != 0 ? p.bias[col] : 0.0f;
 #pragma unroll
     for (int i = 0; i < kFM; ++i) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
         float v = acc[i][j][r] + bv;
-        if (p.epi == 2) v = relu_f32(v);
-        store_from_f32(C + (int64_t)row * p.ldc + col, v);
+        if ((p.epi & kEpiOpMask) == 2) v = relu_f32(v);
+        store_from_f32(C + (int64_t)row * p.ldc + col, v, trunc16);
       }
     }
   }

@@ -20,8 +20,11 @@ struct GemmDesc {
   int64_t ldc;
   bool in_bf16, out_bf16;
   const float* bias;
-  int epi;  // 0 none, 1 bias, 2 bias + relu
+  int epi;  // (epi & kEpiOpMask): 0 none, 1 bias, 2 bias + relu; kEpiTrunc16: truncating 16-bit output
 };
+
+constexpr int kEpiOpMask = 3;
+constexpr int kEpiTrunc16 = 16;
 
 bool gemm_vector_ok(const GemmDesc& d, int elem_bytes);
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s);
@@ -50,9 +53,12 @@ size_t softmax_xent_ws_bytes(int64_t rows);
 hipError_t launch_softmax_xent(const void* logits, const int32_t* labels, void* grad, double* loss, int64_t rows,
                                int64_t cols, bool bf16, void* ws, hipStream_t s);
 
-hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow,
+hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow, bool trunc,
                       hipStream_t s);
 hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,
-                             uint16_t* shadow, uint16_t* shadow_t, hipStream_t s);
+                             uint16_t* shadow, uint16_t* shadow_t, bool trunc, hipStream_t s);
+
+hipError_t launch_convert_to_bf16(const float* src, uint16_t* dst, int64_t count, bool trunc, hipStream_t s);
+hipError_t launch_convert_to_f32(const uint16_t* src, float* dst, int64_t count, hipStream_t s);
 
 }  // namespace tfd

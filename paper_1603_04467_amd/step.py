@@ -81,7 +81,7 @@ class DenseStep:
             for l in range(L):
                 self.dw[l].zero_()
                 T.tfd_apply_gradient_descent_matrix(self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
-                                                    var_bf16_t=self.weights_t[l])
+                                                    var_bf16_t=self.weights_t[l], rounding=w.rounding)
 
         # pristine copies of the Variables, to restart from the same state
         self._saved = [t.clone() for t in self.variables()]
@@ -110,9 +110,10 @@ class DenseStep:
             epi = "bias_relu" if w.relus[l] else "bias"
             if self.weights_t is not None:
                 T.tfd_matmul(self.h[l], self.weights_t[l], self.h[l + 1], transpose_b=True, bias=self.biases[l],
-                             epilogue=epi)
+                             epilogue=epi, rounding=w.rounding)
             else:
-                T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l], epilogue=epi)
+                T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l], epilogue=epi,
+                             rounding=w.rounding)
         if self.upstream is None:
             if mark:
                 mark("loss")
@@ -132,7 +133,7 @@ class DenseStep:
                 dyl = grad
             if mark:
                 mark(f"dx{l + 1}")
-            T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True)
+            T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding)
             if mark:
                 mark(f"dw{l + 1}")
             T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True)
@@ -141,7 +142,7 @@ class DenseStep:
                     mark(f"sgd{l + 1}")
                 if self.masters is not None:
                     T.tfd_apply_gradient_descent_matrix(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l],
-                                                        var_bf16_t=self.weights_t[l])
+                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding)
                 else:
                     T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l])
                 T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l])

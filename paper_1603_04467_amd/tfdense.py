@@ -24,13 +24,17 @@ LIB_PATH = os.environ.get("TFD_LIBRARY") or os.path.join(_HERE, "libtfdense.so")
 
 TFD_OK, TFD_EINVAL, TFD_EUNSUPPORTED, TFD_EHIP = 0, 1, 2, 3
 TFD_F32, TFD_BF16 = 0, 1
+TFD_ROUND_NEAREST_EVEN, TFD_ROUND_TRUNCATE = 0, 1
+TFD_EPI_TRUNCATE_16 = 16
+ROUNDINGS = {"nearest": TFD_ROUND_NEAREST_EVEN, "truncate": TFD_ROUND_TRUNCATE}
 EPILOGUES = {"none": 0, "bias": 1, "bias_relu": 2}
 
 EXPORTS = (
     "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
     "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
     "tfd_relu_grad_bias_add_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
-    "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent", "tfd_apply_gradient_descent_matrix",
+    "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent",
+    "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
 )
 
 
@@ -68,8 +72,10 @@ def load() -> ctypes.CDLL:
         "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
         "tfd_softmax_xent_workspace_size": ([i64], sz),
         "tfd_softmax_cross_entropy_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
-        "tfd_apply_gradient_descent": ([vp, ctypes.c_float, vp, i64, vp, vp], i32),
-        "tfd_apply_gradient_descent_matrix": ([vp, ctypes.c_float, vp, i64, i64, vp, vp, vp], i32),
+        "tfd_apply_gradient_descent": ([vp, ctypes.c_float, vp, i64, vp, i32, vp], i32),
+        "tfd_apply_gradient_descent_matrix": ([vp, ctypes.c_float, vp, i64, i64, vp, vp, i32, vp], i32),
+        "tfd_convert_f32_to_bf16": ([vp, vp, i64, i32, vp], i32),
+        "tfd_convert_bf16_to_f32": ([vp, vp, i64, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -120,8 +126,10 @@ def tfd_abi_version() -> int:
     return load().tfd_abi_version()
 
 
-def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogue="none", stream=None):
-    """c = epilogue(op(a) @ op(b)) (see include/tfdense.h)."""
+def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogue="none", rounding="nearest",
+               stream=None):
+    """c = epilogue(op(a) @ op(b)) (see include/tfdense.h); rounding="truncate"
+    writes a 16-bit c with the truncating converter."""
     lda, ldb, ldc = _rowmajor(a, "a"), _rowmajor(b, "b"), _rowmajor(c, "c")
     m = a.size(1) if transpose_a else a.size(0)
     k = a.size(0) if transpose_a else a.size(1)
@@ -133,7 +141,8 @@ def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogu
         raise ValueError("bias must be a contiguous fp32 vector of length n")
     _check(load().tfd_matmul(int(transpose_a), int(transpose_b), m, n, k,
                              _ptr(a), lda, _dtype(a), _ptr(b), ldb, _dtype(b), _ptr(c), ldc, _dtype(c),
-                             _ptr(bias), EPILOGUES[epilogue], _stream(stream)))
+                             _ptr(bias), EPILOGUES[epilogue] | (TFD_EPI_TRUNCATE_16 if ROUNDINGS[rounding] else 0),
+                             _stream(stream)))
     return c
 
 
@@ -224,18 +233,19 @@ def tfd_softmax_cross_entropy_grad(logits, labels, grad, loss, workspace=None, s
     return grad, loss
 
 
-def tfd_apply_gradient_descent(var, alpha, delta, var_bf16=None, stream=None):
+def tfd_apply_gradient_descent(var, alpha, delta, var_bf16=None, rounding="nearest", stream=None):
     n = _flat(var, "var")
     if var.dtype != torch.float32 or delta.dtype != torch.float32:
         raise TypeError("Variables and their deltas are fp32")
     if var_bf16 is not None and var_bf16.dtype != torch.bfloat16:
         raise TypeError("the 16-bit copy must be bfloat16")
     _check(load().tfd_apply_gradient_descent(_ptr(var), float(alpha), _ptr(delta), n, _ptr(var_bf16),
-                                             _stream(stream)))
+                                             ROUNDINGS[rounding], _stream(stream)))
     return var
 
 
-def tfd_apply_gradient_descent_matrix(var, alpha, delta, var_bf16=None, var_bf16_t=None, stream=None):
+def tfd_apply_gradient_descent_matrix(var, alpha, delta, var_bf16=None, var_bf16_t=None, rounding="nearest",
+                                      stream=None):
     """var[rows, cols] -= alpha * delta (one rounding), refreshing the 16-bit
     copies var_bf16 [rows, cols] and var_bf16_t [cols, rows] when given."""
     if var.dim() != 2 or not var.is_contiguous() or var.dtype != torch.float32:
@@ -247,5 +257,25 @@ def tfd_apply_gradient_descent_matrix(var, alpha, delta, var_bf16=None, var_bf16
         if t is not None and (t.dtype != torch.bfloat16 or tuple(t.shape) != shape or not t.is_contiguous()):
             raise ValueError("16-bit copies must be contiguous bfloat16 of the matching shape")
     _check(load().tfd_apply_gradient_descent_matrix(_ptr(var), float(alpha), _ptr(delta), rows, cols,
-                                                    _ptr(var_bf16), _ptr(var_bf16_t), _stream(stream)))
+                                                    _ptr(var_bf16), _ptr(var_bf16_t), ROUNDINGS[rounding],
+                                                    _stream(stream)))
     return var
+
+
+def tfd_convert_f32_to_bf16(src, dst, rounding="truncate", stream=None):
+    """dst (bfloat16) = src (fp32) through the 32 -> 16-bit converter;
+    rounding "truncate" (the default: the lossy converter) or "nearest"."""
+    n = _flat(src, "src")
+    if src.dtype != torch.float32 or dst.dtype != torch.bfloat16 or dst.numel() != n or not dst.is_contiguous():
+        raise ValueError("src must be fp32 and dst contiguous bfloat16 of the same size")
+    _check(load().tfd_convert_f32_to_bf16(_ptr(src), _ptr(dst), n, ROUNDINGS[rounding], _stream(stream)))
+    return dst
+
+
+def tfd_convert_bf16_to_f32(src, dst, stream=None):
+    """dst (fp32) = src (bfloat16) with the low 16 bits zero."""
+    n = _flat(src, "src")
+    if src.dtype != torch.bfloat16 or dst.dtype != torch.float32 or dst.numel() != n or not dst.is_contiguous():
+        raise ValueError("src must be bfloat16 and dst contiguous fp32 of the same size")
+    _check(load().tfd_convert_bf16_to_f32(_ptr(src), _ptr(dst), n, _stream(stream)))
+    return dst

@@ -36,6 +36,9 @@ class Workload:
     uniformly from [0, d_L)) or "upstream" (a given upstream gradient ~ N(0,1)).
     ``masters``: the updated fp32 Variables are separate from the 16-bit
     GEMM operands.
+    ``rounding``: how 16-bit activations, input gradients and weight copies
+    are produced from fp32: "nearest" (even) or "truncate" (the lossy
+    converter of section 5.5).
     """
     name: str
     wid: int
@@ -50,6 +53,7 @@ class Workload:
     lr: float = 0.01
     update: bool = True
     masters: bool = False
+    rounding: str = "nearest"
 
     @property
     def layers(self):
@@ -95,6 +99,12 @@ WORKLOADS = {
         name="wide4096x4-bf16", wid=3, batch=16384, dims=(4096,) * 5,
         relus=(True, True, True, False), act="bf16", input_dist="normal",
         weight_init=("normal", 1.0 / 64.0), bias_init=("zero",), cost="sq_err", masters=True),
+    # same inputs as wide4096x4-bf16 (same workload id), truncating conversions
+    "wide4096x4-bf16-trunc": Workload(
+        name="wide4096x4-bf16-trunc", wid=3, batch=16384, dims=(4096,) * 5,
+        relus=(True, True, True, False), act="bf16", input_dist="normal",
+        weight_init=("normal", 1.0 / 64.0), bias_init=("zero",), cost="sq_err", masters=True,
+        rounding="truncate"),
     "tall512x32768-bf16": Workload(
         name="tall512x32768-bf16", wid=4, batch=16384, dims=(512, 32768), relus=(True,),
         act="bf16", input_dist="normal", weight_init=("normal", 0.02), bias_init=("normal", 0.01),

@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.tfd_abi_version() == 1
+    assert lib.tfd_abi_version() == 2
     assert lib.tfd_status_string(0) == b"ok"
     assert lib.tfd_status_string(1) == b"invalid argument"
     assert lib.tfd_status_string(2) == b"unsupported"
@@ -97,5 +97,33 @@ def test_elementwise_and_reduction_validation(lib):
     lneed = lib.tfd_loss_workspace_size(1000, 0)
     assert lneed >= 8
     assert lib.tfd_l2_loss_grad(FAKE, None, FAKE * 2, None, 1000, 0, FAKE * 3, lneed, None) == 1
-    assert lib.tfd_apply_gradient_descent(FAKE, ctypes.c_float(0.01), FAKE + 8, 100, None, None) == 1
-    assert lib.tfd_apply_gradient_descent(None, ctypes.c_float(0.01), None, 0, None, None) == 0
+    assert lib.tfd_apply_gradient_descent(FAKE, ctypes.c_float(0.01), FAKE + 8, 100, None, 0, None) == 1
+    assert lib.tfd_apply_gradient_descent(None, ctypes.c_float(0.01), None, 0, None, 0, None) == 0
+
+
+def test_softmax_and_conversion_validation(lib):
+    sneed = lib.tfd_softmax_xent_workspace_size(1000)
+    assert sneed >= 8 and lib.tfd_softmax_xent_workspace_size(-1) == 0
+    xent = lib.tfd_softmax_cross_entropy_grad
+    assert xent(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, -1, 10, 0, FAKE * 5, sneed, None) == 1
+    assert xent(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 1000, 0, 0, FAKE * 5, sneed, None) == 1   # no classes
+    assert xent(FAKE, FAKE * 2, FAKE * 3, None, 1000, 10, 0, FAKE * 5, sneed, None) == 1      # no loss
+    assert xent(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 1000, 10, 0, FAKE * 5, sneed - 1, None) == 1
+    assert b"workspace" in lib.tfd_last_error()
+    assert xent(FAKE, FAKE * 2, FAKE + 64, FAKE * 4, 1000, 10, 0, FAKE * 5, sneed, None) == 1  # grad aliases
+    assert b"overlap" in lib.tfd_last_error()
+    # conversions: negative count, unknown rounding, overlap, empty no-op
+    assert lib.tfd_convert_f32_to_bf16(FAKE, FAKE * 2, -1, 1, None) == 1
+    assert lib.tfd_convert_f32_to_bf16(FAKE, FAKE * 2, 10, 7, None) == 1
+    assert lib.tfd_convert_f32_to_bf16(FAKE, FAKE + 8, 10, 1, None) == 1
+    assert lib.tfd_convert_f32_to_bf16(None, None, 0, 1, None) == 0
+    assert lib.tfd_convert_bf16_to_f32(FAKE, FAKE + 8, 10, None) == 1
+    assert lib.tfd_convert_bf16_to_f32(None, FAKE, 10, None) == 1
+    # the truncating epilogue flag needs a 16-bit output; unknown SGD rounding
+    mm = lib.tfd_matmul
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 16, None) == 1
+    assert b"16-bit" in lib.tfd_last_error()
+    assert mm(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 3 | 16, None) == 1
+    assert lib.tfd_apply_gradient_descent(FAKE, ctypes.c_float(0.01), FAKE * 2, 100, None, 5, None) == 1
+    assert lib.tfd_apply_gradient_descent_matrix(FAKE, ctypes.c_float(0.01), FAKE * 2, 10, 10, None, None, 5,
+                                                 None) == 1

@@ -30,11 +30,21 @@ from tests.parity import TAU, amax, assert_bits, assert_close, to_f64
 pytestmark = pytest.mark.gpu
 
 
+def _store(w):
+    """Oracle storage type of the step's 16-bit activations and weight copies."""
+    return "bf16t" if w.rounding == "truncate" else w.act
+
+
 def _host_inputs(w, inp):
     conv = oracle.bf16_bits_to_f64 if w.act == "bf16" else (lambda a: a.astype(np.float64))
+    if w.rounding == "truncate":
+        # the 16-bit operand copies are derived from the fp32 masters by the converter
+        weights = [oracle.round_to(a.astype(np.float64), "bf16t") for a in inp["masters"]]
+    else:
+        weights = [conv(a) for a in inp["weights"]]
     return {
         "x": conv(inp["x"]),
-        "weights": [conv(a) for a in inp["weights"]],
+        "weights": weights,
         "masters": None if inp["masters"] is None else [a.astype(np.float64) for a in inp["masters"]],
         "biases": [a.astype(np.float64) for a in inp["biases"]],
         "target": None if inp["target"] is None else conv(inp["target"]),
@@ -101,7 +111,7 @@ def _compare_full(w, inp, s):
     L = w.layers
     ref = oracle.dense_step(hi["x"], hi["weights"], hi["biases"], list(w.relus), act=w.act,
                             target=hi["target"], upstream_grad=hi["upstream"], lr=w.lr,
-                            masters=hi["masters"], update=w.update, labels=hi["labels"])
+                            masters=hi["masters"], update=w.update, labels=hi["labels"], rounding=w.rounding)
     h_gpu = [to_f64(t) for t in s.h]
     # forward
     D_fwd = []
@@ -164,7 +174,12 @@ def _compare_full(w, inp, s):
                 assert torch.equal(s.weights_t[l], s.weights[l].t()), f"W^T_{l + 1} is not the transposed copy"
                 mw = amax(ref["new_masters"][l])
                 _assert_within(to_f64(s.masters[l]), ref["new_masters"][l], allowed_w + 2.0 ** -23 * mw, f"W_{l + 1}")
-                _assert_within(to_f64(s.weights[l]), ref["new_weights"][l], allowed_w + 2.0 ** -8 * mw, f"W16_{l + 1}")
+                # one 16-bit step: half of one under nearest even, a whole one under truncation
+                step16 = 2.0 ** -7 if w.rounding == "truncate" else 2.0 ** -8
+                _assert_within(to_f64(s.weights[l]), ref["new_weights"][l], allowed_w + step16 * mw, f"W16_{l + 1}")
+                # the copy is exactly the GPU's own updated master through the converter
+                own = oracle.round_to(to_f64(s.masters[l]), _store(w))
+                assert_bits(to_f64(s.weights[l]), own, f"W16_{l + 1} from the updated master")
             else:
                 mw = amax(ref["new_weights"][l])
                 _assert_within(to_f64(s.weights[l]), ref["new_weights"][l], allowed_w + 2.0 ** -23 * mw, f"W_{l + 1}")
@@ -185,6 +200,8 @@ SCALED = [
     ("wide4096x4-f32", 520, (136, 256, 512, 264, 128)),
     ("wide4096x4-bf16", 600, (256, 384, 264, 128, 200)),
     ("wide4096x4-bf16", 1032, (512, 768, 512, 256, 512)),
+    ("wide4096x4-bf16-trunc", 600, (256, 384, 264, 128, 200)),
+    ("wide4096x4-bf16-trunc", 1032, (512, 768, 512, 256, 512)),
     ("tall512x32768-bf16", 1000, (512, 2048)),
     ("tall512x32768-bf16", 264, (96, 4104)),
     ("tall512x32768-bf16", 130, (100, 1030)),
@@ -245,7 +262,7 @@ def _check_full_size(name):
     for l in range(L):
         D = w.dims[l] * amax(h_ref[l]) * amax(hi["weights"][l]) + amax(hi["biases"][l])
         y = oracle.matmul(h_ref[l], hi["weights"][l], out="f64", bias=hi["biases"][l])
-        h = oracle.round_to(oracle.relu(y) if w.relus[l] else y, w.act)
+        h = oracle.round_to(oracle.relu(y) if w.relus[l] else y, _store(w))
         y_ref.append(y)
         h_ref.append(h)
         D_fwd.append(D)
@@ -265,7 +282,7 @@ def _check_full_size(name):
     assert not w.relus[top]
     md = amax(g_ref)
     mh = amax(h_ref[top])
-    dx_top = oracle.matmul(g_ref, hi["weights"][top], transpose_b=True, out=w.act)
+    dx_top = oracle.matmul(g_ref, hi["weights"][top], transpose_b=True, out=_store(w))
     assert_close(to_f64(s.dx[top]), dx_top, w.dims[-1] * md * amax(hi["weights"][top]), tau, f"dX_{L}")
     assert_close(to_f64(s.dw[top]), oracle.matmul(h_ref[top], g_ref, transpose_a=True, out="f32"),
                  w.batch * mh * md, tau, f"dW_{L}")
@@ -278,7 +295,7 @@ def _check_full_size(name):
     for l in reversed(range(top)):
         dy_rows = oracle.relu_grad(g_rows, h_ref[l + 1][rows])
         assert_close(to_f64(s.dy[l])[rows], dy_rows, D_g, tau, f"dY_{l + 1} (sampled rows)")
-        dx_rows = oracle.matmul(dy_rows, hi["weights"][l], transpose_b=True, out=w.act)
+        dx_rows = oracle.matmul(dy_rows, hi["weights"][l], transpose_b=True, out=_store(w))
         D_dx = w.dims[l + 1] * amax(dy_rows) * amax(hi["weights"][l])
         assert_close(to_f64(s.dx[l])[rows], dx_rows, D_dx, tau, f"dX_{l + 1} (sampled rows)")
         g_rows, D_g = dx_rows, D_dx
@@ -289,7 +306,8 @@ def _check_full_size(name):
     return int(touched.sum())
 
 
-@pytest.mark.parametrize("name", ["wide4096x4-f32", "wide4096x4-bf16", "tall512x32768-bf16"])
+@pytest.mark.parametrize("name", ["wide4096x4-f32", "wide4096x4-bf16", "wide4096x4-bf16-trunc",
+                                  "tall512x32768-bf16"])
 def test_full_size_step(name):
     flips = _check_full_size(name)
     print(f"{name}: {flips} rows with in-band Relu mask differences")
