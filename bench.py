@@ -37,6 +37,9 @@ METRIC = "TFLOP/s per dense-layer fwd+bwd+SGD step; % of MI355X MFMA peak"
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA peaks (256 CUs x 2.4 GHz)
 HBM_PEAK_GBS = 8000.0
 PRIMARY = "wide4096x4-bf16"
+# steps too small to fill the GPU with one kernel at a time: also timed with
+# concurrent streams and HIP graph replay
+LAUNCH_BOUND = ("mlp784-1024-1024-10-xent", "mlp784-1024-1024-10", "dense784x100")
 # timed in the same run and reported under "also": the fp32 twin, then the
 # MNIST-shaped steps (classifier head and squared-error head) and the single layer
 SECONDARY = ("wide4096x4-f32", "wide4096x4-bf16-trunc", "mlp784-1024-1024-10-xent", "mlp784-1024-1024-10",
@@ -241,6 +244,47 @@ def cpu_baseline(name: str, rows: int):
     }
 
 
+def time_modes(name: str, steps: int, warmup: int, num_streams: int = 3):
+    """Step time of one workload under four launch modes: one stream in
+    program order ("serial"), independent ops on `num_streams` streams
+    ("streams"), and both captured into a HIP graph and replayed ("graph",
+    "graph_streams"). Every step starts from the same Variables (restore
+    outside the timed interval); times are HIP-event means in ms."""
+    import torch
+
+    from paper_1603_04467_amd import workloads
+    from paper_1603_04467_amd.step import DenseStep
+
+    w = workloads.workload(name)
+    s = DenseStep(w, workloads.generate(w, seed=0))
+    stream = torch.cuda.current_stream()
+    graphs = {"graph": s.capture(concurrent=False), "graph_streams": s.capture(concurrent=True,
+                                                                               num_streams=num_streams)}
+    modes = {
+        "serial": s.run,
+        "streams": lambda: s.run_concurrent(num_streams),
+        "graph": graphs["graph"].replay,
+        "graph_streams": graphs["graph_streams"].replay,
+    }
+    out = {}
+    for mode, fn in modes.items():
+        for _ in range(warmup):
+            s.restore()
+            fn()
+        ev = []
+        for _ in range(steps):
+            s.restore()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            ev.append((a, b))
+        torch.cuda.synchronize()
+        out[mode] = round(float(np.mean([a.elapsed_time(b) for a, b in ev])), 4)
+    best = min(out, key=out.get)
+    return {"ms_per_step": out, "best": best, "tflops_best": round(w.flops() / (out[best] * 1e-3) / 1e12, 3)}
+
+
 def time_conversions(count: int = 1 << 26, reps: int = 20):
     """The 32 <-> 16-bit conversion ops of section 5.5 on `count` elements
     (fp32 -> 16 truncating and nearest even, 16 -> fp32), resident in HBM:
@@ -355,6 +399,8 @@ def main():
                 "per_op": _per_op(r2["ops"]),
                 "loss": r2["loss"],
             })
+            if name in LAUNCH_BOUND:
+                out["also"][-1]["launch_modes"] = time_modes(name, args.steps, args.warmup)
     if not args.no_secondary and args.workload == PRIMARY:
         print("bench: timing the 32 <-> 16-bit conversions", file=sys.stderr, flush=True)
         out["conversions"] = time_conversions()

@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtfdense.so")
 
-SOURCES = ["gemm.hip", "gemm_bf16.hip", "elementwise.hip", "reduce.hip", "softmax.hip", "convert.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "gemm_bf16.hip", "gemm_small.hip", "elementwise.hip", "reduce.hip", "softmax.hip", "convert.hip", "api.cpp"]
 
 ARCH = "gfx950"
 FLAGS = [

@@ -327,8 +327,10 @@ hipError_t launch_cfg(const GemmDesc& d, hipStream_t s) {
 // 1 = 256x256 (4 waves of 128x128), 2 = 256x128 (4 waves of 128x64),
 // 3 = 128x128 (4 waves of 64x64), 4 = 64x64 (4 waves of 32x32); fp32 only:
 // 5 = 256x256 (8 waves of 128x64), 6 = 256x256 (16 waves of 64x64),
-// 7 = 128x128 (8 waves of 64x32). Non-zero values come from the tuning-only
-// environment variable TFD_GEMM_TILE.
+// 7 = 128x128 (8 waves of 64x32), 8 = the small-problem kernel of
+// gemm_small.hip (the default for fp32 problems with fewer than 128 tiles of
+// 128 x 128). Non-zero values come from the tuning-only environment variable
+// TFD_GEMM_TILE.
 template <typename T, typename OutT, bool TA, bool TB>
 hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t s) {
   if (!aligned) return launch_cfg<T, OutT, TA, TB, 64, 64, 2, 2, false>(d, s);
@@ -382,6 +384,7 @@ bool gemm_vector_ok(const GemmDesc& d, int elem_bytes) {
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s) {
   const int tile = tile_override();
   if (tile == 0 && gemm_bf16_256_ok(d)) return launch_gemm_bf16_256(d, s);
+  if (!d.in_bf16 && (tile == 8 || (tile == 0 && gemm_small_preferred(d)))) return launch_gemm_small_f32(d, s);
   if (d.in_bf16) {
     const bool aligned = gemm_vector_ok(d, 2);
     return d.out_bf16 ? launch_types<bf16, bf16>(d, aligned, tile, s)

@@ -31,6 +31,9 @@ hipError_t launch_gemm(const GemmDesc& d, hipStream_t s);
 // 16-bit operands, whole 256 x 256 tiles, k a multiple of 64 (gemm_bf16.hip).
 bool gemm_bf16_256_ok(const GemmDesc& d);
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s);
+// fp32 problems too small to fill the GPU with 128 x 128 tiles (gemm_small.hip).
+bool gemm_small_preferred(const GemmDesc& d);
+hipError_t launch_gemm_small_f32(const GemmDesc& d, hipStream_t s);
 
 hipError_t launch_bias_add(const void* value, const float* bias, void* out, int64_t rows, int64_t cols,
                            bool bf16, hipStream_t s);

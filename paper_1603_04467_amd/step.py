@@ -35,6 +35,28 @@ def _to_device(a: np.ndarray, act: str, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
+def op_graph(w: Workload):
+    """(name, reads, writes) of every op of one step of ``w``, in program
+    order. Keys name buffers: h<l> activations (h0 = x), g the cost gradient,
+    dy<l>/dx<l>/dw<l>/db<l> the gradients of layer l, W<l>/b<l> its Variables
+    (all copies of the weights), ws the shared reduction workspace."""
+    L = w.layers
+    ops = [(f"fwd{l + 1}", (f"h{l}", f"W{l}", f"b{l}"), (f"h{l + 1}",)) for l in range(L)]
+    if w.cost != "upstream":
+        ops.append(("loss", (f"h{L}", "target"), ("g", "loss", "ws")))
+    gkey = "g"
+    for l in reversed(range(L)):
+        dykey = f"dy{l}" if w.relus[l] else gkey
+        rg_writes = (f"dy{l}", f"db{l}", "ws") if w.relus[l] else (f"db{l}", "ws")
+        ops.append((f"relugrad{l + 1}", (gkey, f"h{l + 1}"), rg_writes))
+        ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}",)))
+        ops.append((f"dw{l + 1}", (f"h{l}", dykey), (f"dw{l}",)))
+        if w.update:
+            ops.append((f"sgd{l + 1}", (f"dw{l}", f"db{l}"), (f"W{l}", f"b{l}")))
+        gkey = f"dx{l}"
+    return ops
+
+
 class DenseStep:
     """Device state and launch sequence of one step of workload ``w``."""
 
@@ -99,56 +121,109 @@ class DenseStep:
         for t, s in zip(self.variables(), self._saved):
             t.copy_(s)
 
-    def run(self, mark=None):
-        """Enqueue one step. ``mark(name)`` (optional) is called between
-        launches, e.g. to record timing events."""
+    def nodes(self):
+        """The step's op nodes in program order (op_graph), each with the
+        launch of its kernels on a given stream."""
+        from .executor import Node
+
         w, L = self.w, self.w.layers
         ws = self.workspace
-        for l in range(L):
-            if mark:
-                mark(f"fwd{l + 1}")
+        launches = {}
+
+        def fwd(l):
             epi = "bias_relu" if w.relus[l] else "bias"
-            if self.weights_t is not None:
-                T.tfd_matmul(self.h[l], self.weights_t[l], self.h[l + 1], transpose_b=True, bias=self.biases[l],
-                             epilogue=epi, rounding=w.rounding)
-            else:
-                T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l], epilogue=epi,
-                             rounding=w.rounding)
-        if self.upstream is None:
-            if mark:
-                mark("loss")
+
+            def launch(st):
+                if self.weights_t is not None:
+                    T.tfd_matmul(self.h[l], self.weights_t[l], self.h[l + 1], transpose_b=True, bias=self.biases[l],
+                                 epilogue=epi, rounding=w.rounding, stream=st)
+                else:
+                    T.tfd_matmul(self.h[l], self.weights[l], self.h[l + 1], bias=self.biases[l], epilogue=epi,
+                                 rounding=w.rounding, stream=st)
+            return launch
+
+        for l in range(L):
+            launches[f"fwd{l + 1}"] = fwd(l)
+
+        def loss(st):
             if self.labels is not None:
-                T.tfd_softmax_cross_entropy_grad(self.h[L], self.labels, self.g, self.loss, workspace=ws)
+                T.tfd_softmax_cross_entropy_grad(self.h[L], self.labels, self.g, self.loss, workspace=ws, stream=st)
             else:
-                T.tfd_l2_loss_grad(self.h[L], self.target, self.g, self.loss, workspace=ws)
-        grad = self.g
-        for l in reversed(range(L)):
-            if mark:
-                mark(f"relugrad{l + 1}")
-            if w.relus[l]:
-                T.tfd_relu_grad_bias_add_grad(grad, self.h[l + 1], self.dy[l], self.db[l], workspace=ws)
-                dyl = self.dy[l]
-            else:
-                T.tfd_bias_add_grad(grad, self.db[l], workspace=ws)
-                dyl = grad
-            if mark:
-                mark(f"dx{l + 1}")
-            T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding)
-            if mark:
-                mark(f"dw{l + 1}")
-            T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True)
-            if w.update:
-                if mark:
-                    mark(f"sgd{l + 1}")
+                T.tfd_l2_loss_grad(self.h[L], self.target, self.g, self.loss, workspace=ws, stream=st)
+        launches["loss"] = loss
+
+        def backward(l, grad):
+            dyl = self.dy[l] if w.relus[l] else grad
+
+            def relugrad(st):
+                if w.relus[l]:
+                    T.tfd_relu_grad_bias_add_grad(grad, self.h[l + 1], self.dy[l], self.db[l], workspace=ws, stream=st)
+                else:
+                    T.tfd_bias_add_grad(grad, self.db[l], workspace=ws, stream=st)
+
+            def dx(st):
+                T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding, stream=st)
+
+            def dw(st):
+                T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True, stream=st)
+
+            def sgd(st):
                 if self.masters is not None:
                     T.tfd_apply_gradient_descent_matrix(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l],
-                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding)
+                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding, stream=st)
                 else:
-                    T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l])
-                T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l])
+                    T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l], stream=st)
+                T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l], stream=st)
+
+            launches.update({f"relugrad{l + 1}": relugrad, f"dx{l + 1}": dx, f"dw{l + 1}": dw, f"sgd{l + 1}": sgd})
+
+        grad = self.g
+        for l in reversed(range(L)):
+            backward(l, grad)
             grad = self.dx[l]
+        return [Node(name, launches[name], reads, writes) for name, reads, writes in op_graph(w)]
+
+    def run(self, mark=None, stream=None):
+        """Enqueue one step in program order on one stream (the current one
+        by default). ``mark(name)`` (optional) is called between launches,
+        e.g. to record timing events."""
+        st = stream or torch.cuda.current_stream()
+        for n in self.nodes():
+            if mark:
+                mark(n.name)
+            n.launch(st)
         if mark:
             mark("end")
+
+    def executor(self, num_streams=3):
+        """A StreamExecutor over this step's op graph (cached per stream count)."""
+        from .executor import StreamExecutor
+
+        cache = self.__dict__.setdefault("_executors", {})
+        if num_streams not in cache:
+            cache[num_streams] = StreamExecutor(self.nodes(), num_streams=num_streams, device=self.device)
+        return cache[num_streams]
+
+    def run_concurrent(self, num_streams=3):
+        """Enqueue one step with independent ops on separate streams, forked
+        from and joined back to the current stream."""
+        self.executor(num_streams).enqueue(torch.cuda.current_stream())
+
+    def capture(self, concurrent=True, num_streams=3):
+        """Record one step into a HIP graph (torch.cuda.CUDAGraph); replaying
+        it runs the same kernels on the same buffers. The library's calls
+        only launch kernels (no allocation, no memset), so they capture."""
+        g = torch.cuda.CUDAGraph()
+        if concurrent:
+            ex = self.executor(num_streams)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            if concurrent:
+                ex.enqueue(torch.cuda.current_stream())
+            else:
+                self.run()
+        torch.cuda.synchronize()
+        return g
 
     def dy_of(self, l: int) -> torch.Tensor:
         """dY of layer l (0-based): the masked gradient, or the incoming

@@ -103,7 +103,7 @@ def test_matmul_parity(m, n, k, layout, din, dout):
         assert bad == 0, f"{bad} Relu mask decisions differ outside the rounding band"
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7, 8])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 @pytest.mark.parametrize("din,dout", TYPES)
 def test_matmul_every_tile_config(tile, layout, din, dout):
