@@ -4,7 +4,8 @@
 //
 // One workgroup per 32x32 output tile, W waves per workgroup, each wave
 // summing a contiguous slice of k with v_mfma_f32_32x32x2_f32 straight from
-// registers (no LDS staging: every operand element is used by one MFMA of one
+// registers, with the next 32 k of operands loaded while the current 32 are
+// multiplied (no LDS staging: every operand element is used by one MFMA of one
 // wave, and the small operands stay in L2). Per 8 values of k a lane loads 4
 // consecutive k of its row of A and of its column of B: 16-byte loads for a
 // k-contiguous operand, 4 coalesced loads for an m/n-contiguous one. The four
@@ -13,8 +14,11 @@
 //
 // The W partial tiles meet in LDS and are added in wave order (a fixed order:
 // results are bitwise reproducible), then the epilogue adds the bias, applies
-// the ReLU and stores. Rows, columns and k beyond the problem are guarded
-// (zeros are summed instead), so any shape and leading dimension works.
+// the ReLU and stores. Lanes past the last row or column read clamped indices
+// (their results are not stored) and k past the end reads zeros, so any
+// shape and leading dimension works.
+
+#include <stdlib.h>
 
 #include "common.h"
 #include "kernels.h"
@@ -35,50 +39,101 @@ struct SmallParams {
   int kper;  // k values per wave, a multiple of 8
 };
 
-// Four consecutive k (kk .. kk+3, clipped at ke) of row r of a k-contiguous
-// operand X (X[r * ld + k]).
-template <bool VEC>
-__device__ __forceinline__ f32x4 load_kc(const float* __restrict__ x, int64_t ld, int r, bool r_ok, int kk, int ke) {
-  f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (!r_ok) return v;
-  const float* p = x + (int64_t)r * ld + kk;
-  if (VEC && kk + 4 <= ke) return *reinterpret_cast<const f32x4*>(p);
+// Four consecutive k (kk .. kk+3) of row r of a k-contiguous operand X
+// (X[r * ld + k]). GUARD: k at or past ke reads element ke - 1 and is
+// replaced by zero (branch-free selects; only the last group of a wave's
+// slice needs it).
+template <bool VEC, bool GUARD>
+__device__ __forceinline__ f32x4 load_kc(const float* __restrict__ x, int64_t ld, int r, int kk, int ke) {
+  const float* p = x + (int64_t)r * ld;
+  f32x4 v;
+  if (!GUARD && VEC) return *reinterpret_cast<const f32x4*>(p + kk);
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (kk + j < ke) v[j] = p[j];
+  for (int j = 0; j < 4; ++j) {
+    if (GUARD) {
+      const float t = p[min(kk + j, ke - 1)];
+      v[j] = kk + j < ke ? t : 0.0f;
+    } else {
+      v[j] = p[kk + j];
+    }
+  }
   return v;
 }
 
 // Four consecutive k of column c of an m/n-contiguous operand X (X[k * ld + c]).
-__device__ __forceinline__ f32x4 load_mn(const float* __restrict__ x, int64_t ld, int c, bool c_ok, int kk, int ke) {
-  f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (!c_ok) return v;
+template <bool GUARD>
+__device__ __forceinline__ f32x4 load_mn(const float* __restrict__ x, int64_t ld, int c, int kk, int ke) {
+  f32x4 v;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (kk + j < ke) v[j] = x[(int64_t)(kk + j) * ld + c];
+  for (int j = 0; j < 4; ++j) {
+    if (GUARD) {
+      const float t = x[(int64_t)min(kk + j, ke - 1) * ld + c];
+      v[j] = kk + j < ke ? t : 0.0f;
+    } else {
+      v[j] = x[(int64_t)(kk + j) * ld + c];
+    }
+  }
   return v;
 }
 
-template <bool TA, bool TB, bool VEC>
-__device__ __forceinline__ void load_chunk(const SmallParams& p, int row, bool row_ok, int col, bool col_ok, int kk,
-                                           int ke, f32x4& a, f32x4& b) {
-  a = TA ? load_mn(p.a, p.lda, row, row_ok, kk, ke) : load_kc<VEC>(p.a, p.lda, row, row_ok, kk, ke);
-  b = TB ? load_kc<VEC>(p.b, p.ldb, col, col_ok, kk, ke) : load_mn(p.b, p.ldb, col, col_ok, kk, ke);
+// Row and column indices are clamped into the problem by the caller: a lane
+// past the last row or column computes a copy of an edge value that is never
+// stored, so no load needs a row or column guard.
+template <bool TA, bool TB, bool VEC, bool GUARD>
+__device__ __forceinline__ void load_group(const SmallParams& p, int row, int col, int k0, int h, int ke,
+                                           f32x4 (&a)[4], f32x4 (&b)[4]) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int kk = k0 + 8 * c + 4 * h;
+    a[c] = TA ? load_mn<GUARD>(p.a, p.lda, row, kk, ke) : load_kc<VEC, GUARD>(p.a, p.lda, row, kk, ke);
+    b[c] = TB ? load_kc<VEC, GUARD>(p.b, p.ldb, col, kk, ke) : load_mn<GUARD>(p.b, p.ldb, col, kk, ke);
+  }
 }
+
+// Unguarded loads of whole groups through a per-lane pointer that advances
+// by 32 k per group: k-contiguous operands step by 32 elements, m/n-contiguous
+// ones by 32 rows (the per-element offsets are multiples of the uniform ld).
+template <bool KC, bool VEC>
+struct GroupReader {
+  const float* ptr;
+  int64_t ld;
+  __device__ __forceinline__ GroupReader(const float* x, int64_t ld_, int rc, int k0, int h) : ld(ld_) {
+    ptr = KC ? x + (int64_t)rc * ld_ + k0 + 4 * h : x + (int64_t)(k0 + 4 * h) * ld_ + rc;
+  }
+  __device__ __forceinline__ void read(f32x4 (&v)[4]) const {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      if (KC && VEC) {
+        v[c] = *reinterpret_cast<const f32x4*>(ptr + 8 * c);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[c][j] = KC ? ptr[8 * c + j] : ptr[(int64_t)(8 * c + j) * ld];
+      }
+    }
+  }
+  // to the next group, or stay (the loads are then repeated, harmlessly):
+  // unconditional loads keep the outstanding-load count the same on every
+  // path, so the waits before the MFMAs cover only the older register set
+  __device__ __forceinline__ void advance(bool go) { ptr += go ? (KC ? (int64_t)32 : 32 * ld) : 0; }
+};
 
 __device__ __forceinline__ void mfma4(f32x16& acc, const f32x4& a, const f32x4& b) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc, 0, 0, 0);
 }
 
+// Few waves per SIMD are resident (one workgroup of W waves per tile): the
+// occupancy hint lets the scheduler keep a whole group of loads in flight
+// instead of moving each load next to its MFMA to save registers.
 template <bool TA, bool TB, int W, bool VEC>
-__global__ __launch_bounds__(64 * W) void gemm_small_f32(SmallParams p) {
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(1, 4))) void gemm_small_f32(SmallParams p) {
   __shared__ float part[W * 1024];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // the wave index is uniform across the wave: keep it (and the k slice
+  // bounds derived from it) in scalar registers so the loop is scalar
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, h = lane >> 5;
   const int m0 = (blockIdx.x / p.tiles_n) * 32, n0 = (blockIdx.x % p.tiles_n) * 32;
-  const int row = m0 + l32, col = n0 + l32;
-  const bool row_ok = row < p.m, col_ok = col < p.n;
+  const int row = min(m0 + l32, p.m - 1), col = min(n0 + l32, p.n - 1);
   const int kb = w * p.kper;
   const int ke = min(p.k, kb + p.kper);
 
@@ -86,19 +141,47 @@ __global__ __launch_bounds__(64 * W) void gemm_small_f32(SmallParams p) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
 
+  // whole groups of four chunks (32 k): the loads of group g+1 are issued
+  // before the 16 MFMAs of group g; then one guarded partial group
+  const int kfull = ke > kb ? kb + ((ke - kb) / 32) * 32 : kb;
   int k0 = kb;
-  // four chunks (32 k) per iteration: all loads first, then 16 MFMAs
-  for (; k0 + 32 <= ke; k0 += 32) {
-    f32x4 a[4], b[4];
+  if (k0 < kfull) {
+    // two register sets in turn: the loads into one are in flight while
+    // the MFMAs read the other
+    GroupReader<!TA, VEC> ra(p.a, p.lda, row, kb, h);
+    GroupReader<TB, VEC> rb(p.b, p.ldb, col, kb, h);
+    f32x4 a0[4], b0[4], a1[4], b1[4];
+    ra.read(a0);
+    rb.read(b0);
+    for (;;) {
+      const bool more1 = k0 + 32 < kfull;
+      ra.advance(more1);
+      rb.advance(more1);
+      ra.read(a1);
+      rb.read(b1);
+      // keep the next group's loads ahead of this group's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) load_chunk<TA, TB, VEC>(p, row, row_ok, col, col_ok, k0 + 8 * c + 4 * h, ke, a[c], b[c]);
+      for (int c = 0; c < 4; ++c) mfma4(acc, a0[c], b0[c]);
+      k0 += 32;
+      if (!more1) break;
+      const bool more2 = k0 + 32 < kfull;
+      ra.advance(more2);
+      rb.advance(more2);
+      ra.read(a0);
+      rb.read(b0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) mfma4(acc, a1[c], b1[c]);
+      k0 += 32;
+      if (!more2) break;
+    }
+  }
+  if (k0 < ke) {
+    f32x4 a[4], b[4];
+    load_group<TA, TB, VEC, true>(p, row, col, k0, h, ke, a, b);
 #pragma unroll
     for (int c = 0; c < 4; ++c) mfma4(acc, a[c], b[c]);
-  }
-  for (; k0 < ke; k0 += 8) {
-    f32x4 a, b;
-    load_chunk<TA, TB, VEC>(p, row, row_ok, col, col_ok, k0 + 4 * h, ke, a, b);
-    mfma4(acc, a, b);
   }
 
 #pragma unroll
@@ -137,10 +220,13 @@ hipError_t launch_layout(const SmallParams& p, int waves, bool vec, unsigned gri
 
 }  // namespace
 
-// Small problems: fewer than 128 output tiles of 128 x 128.
+// Small problems: fewer than 128 output tiles of 128 x 128, except weight
+// gradients (transpose_a) with 512 or more 32 x 32 tiles, where the LDS-staged
+// 64 x 64 tiles of gemm.hip were measured faster.
 bool gemm_small_preferred(const GemmDesc& d) {
   const int64_t tiles128 = ((d.m + 127) / 128) * ((d.n + 127) / 128);
-  return !d.in_bf16 && !d.out_bf16 && tiles128 < 128;
+  const int64_t tiles32 = ((d.m + 31) / 32) * ((d.n + 31) / 32);
+  return !d.in_bf16 && !d.out_bf16 && tiles128 < 128 && !(d.ta && tiles32 >= 512);
 }
 
 hipError_t launch_gemm_small_f32(const GemmDesc& d, hipStream_t s) {
@@ -159,10 +245,13 @@ hipError_t launch_gemm_small_f32(const GemmDesc& d, hipStream_t s) {
   const int64_t tiles_m = (d.m + 31) / 32, tiles_n = (d.n + 31) / 32;
   p.tiles_n = (int)tiles_n;
   const int64_t tiles = tiles_m * tiles_n;
-  // about 2048 waves in flight (8 per compute unit), 4 to 16 per tile, but no
-  // more waves than 32-wide slices of k
+  // 4 waves per tile: measured fastest for every MNIST-shaped problem, also
+  // those with only a few tiles (8 or 16 waves per tile were slower)
   int waves = 4;
-  while (waves < 16 && tiles * waves < 2048 && (int64_t)waves * 32 < d.k) waves *= 2;
+  if (const char* e = getenv("TFD_SMALL_WAVES")) {  // tuning-only override: 4, 8 or 16
+    const int v = atoi(e);
+    if (v == 4 || v == 8 || v == 16) waves = v;
+  }
   const int64_t per = (d.k + waves - 1) / waves;
   p.kper = (int)(((per + 7) / 8) * 8);
   if (p.kper == 0) p.kper = 8;
