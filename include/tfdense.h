@@ -164,6 +164,30 @@ TFD_API tfd_status tfd_relu_grad_bias_add_grad(const void* gradients, const void
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
 
+/* Workspace bytes that tfd_matmul_relu_grad_bias_add_grad needs for an m x n output. */
+TFD_API size_t tfd_matmul_relu_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type);
+
+/*
+ * The input-gradient MatMul of a dense layer fused with the ReluGrad and
+ * BiasAddGrad of the layer below it (section 4.1: the gradient flows through
+ * the upper layer's MatMul into the lower layer's Relu and Add):
+ *   G[r, c]         = (op(A) op(B))[r, c], fp32 accumulation, rounded once to
+ *                     `type` (with `rounding` for 16-bit outputs); not stored,
+ *   backprops[r, c] = features[r, c] > 0 ? G[r, c] : +0,
+ *   bias_grad[c]    = sum_r backprops[r, c]   (fp32, in a fixed order).
+ * Operands as in tfd_matmul (transpose flags, leading dimensions; A and B of
+ * `type`); features and backprops are m x n of `type`, contiguous (ld = n).
+ * backprops equals what tfd_matmul followed by tfd_relu_grad_bias_add_grad
+ * stores, bit for bit; bias_grad may differ from that path in the order of
+ * its sum. backprops must not overlap A, B, features, bias_grad or the
+ * workspace. TFD_EUNSUPPORTED as for tfd_matmul.
+ */
+TFD_API tfd_status tfd_matmul_relu_grad_bias_add_grad(int transpose_a, int transpose_b, int64_t m, int64_t n,
+                                              int64_t k, const void* a, int64_t lda, const void* b,
+                                              int64_t ldb, const void* features, void* backprops,
+                                              float* bias_grad, tfd_dtype type, tfd_rounding rounding,
+                                              void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace bytes that tfd_l2_loss_grad needs for `count` elements. */
 TFD_API size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type);
 

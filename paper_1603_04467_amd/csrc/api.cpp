@@ -200,6 +200,86 @@ tfd_status tfd_bias_add_grad(const void* out_backprop, float* bias_grad, int64_t
   return st;
 }
 
+size_t tfd_matmul_relu_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type) {
+  if (m < 0 || n < 0 || !valid_dtype(type)) return 0;
+  const size_t fused = (size_t)((m + 255) / 256) * (size_t)n * sizeof(float);
+  const size_t plain = tfd::reduction_ws_bytes(m, n, type == TFD_BF16);
+  return fused > plain ? fused : plain;
+}
+
+tfd_status tfd_matmul_relu_grad_bias_add_grad(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                              const void* a, int64_t lda, const void* b, int64_t ldb,
+                                              const void* features, void* backprops, float* bias_grad,
+                                              tfd_dtype type, tfd_rounding rounding, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: negative size");
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: unknown element type");
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: unknown rounding");
+  if (rounding == TFD_ROUND_TRUNCATE && type != TFD_BF16)
+    return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: truncation needs a 16-bit output");
+  if (transpose_a && transpose_b)
+    return fail(TFD_EUNSUPPORTED, "tfd_matmul_relu_grad_bias_add_grad: transpose_a and transpose_b together");
+  if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30))
+    return fail(TFD_EUNSUPPORTED, "tfd_matmul_relu_grad_bias_add_grad: dimension above 2^30");
+  const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
+  const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
+  if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1))
+    return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: leading dimension smaller than the row");
+  if (n == 0) return TFD_OK;
+  if (!bias_grad) return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: bias_grad is NULL");
+  const size_t need = tfd_matmul_relu_grad_workspace_size(m, n, type);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: workspace of %zu bytes needed, %zu given", need,
+                workspace_bytes);
+  if (m > 0 && (!features || !backprops || (k > 0 && (!a || !b))))
+    return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: NULL pointer");
+  const int eb = elem_bytes(type);
+  const size_t c_span = (size_t)m * (size_t)n * eb;
+  if (overlaps(backprops, c_span, a, span(a_rows, a_cols, lda, eb)) ||
+      overlaps(backprops, c_span, b, span(b_rows, b_cols, ldb, eb)) || overlaps(backprops, c_span, features, c_span) ||
+      overlaps(backprops, c_span, bias_grad, (size_t)n * 4) || overlaps(backprops, c_span, workspace, need) ||
+      overlaps(bias_grad, (size_t)n * 4, workspace, need) || overlaps(bias_grad, (size_t)n * 4, features, c_span))
+    return fail(TFD_EINVAL, "tfd_matmul_relu_grad_bias_add_grad: overlapping buffers");
+  hipStream_t st = as_stream(stream);
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.a = a;
+  d.lda = lda;
+  d.b = b;
+  d.ldb = ldb;
+  d.c = backprops;
+  d.ldc = n;
+  d.in_bf16 = type == TFD_BF16;
+  d.out_bf16 = type == TFD_BF16;
+  d.bias = nullptr;
+  d.epi = rounding == TFD_ROUND_TRUNCATE ? tfd::kEpiTrunc16 : 0;
+  d.features = features;
+  d.ldf = n;
+  d.col_partial = static_cast<float*>(workspace);
+  if (m > 0 && tfd::gemm_bf16_256_ok(d) && tfd::gemm_tile_override() == 0) {
+    hipError_t e = tfd::launch_gemm_bf16_256(d, st);
+    if (e != hipSuccess) return hip_status(e, "tfd_matmul_relu_grad_bias_add_grad launch");
+    return hip_status(tfd::launch_colsum_final(static_cast<const float*>(workspace), bias_grad, m / 256, n, st),
+                      "tfd_matmul_relu_grad_bias_add_grad launch");
+  }
+  // other shapes: the MatMul writes G into backprops, then ReluGrad and
+  // BiasAddGrad run in place over it
+  d.features = nullptr;
+  d.col_partial = nullptr;
+  if (m > 0) {
+    hipError_t e = tfd::launch_gemm(d, st);
+    if (e != hipSuccess) return hip_status(e, "tfd_matmul_relu_grad_bias_add_grad launch");
+  }
+  return hip_status(tfd::launch_relu_grad_bias_add_grad(backprops, features, backprops, bias_grad, m, n,
+                                                        type == TFD_BF16, workspace, st),
+                    "tfd_matmul_relu_grad_bias_add_grad launch");
+}
+
 size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type) {
   if (count < 0 || !valid_dtype(type)) return 0;
   return tfd::loss_ws_bytes(count, type == TFD_BF16);

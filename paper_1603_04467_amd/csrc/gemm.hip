@@ -363,12 +363,12 @@ hipError_t launch_types(const GemmDesc& d, bool aligned, int tile, hipStream_t s
   return launch_layout<T, OutT, true, false>(d, aligned, tile, s);
 }
 
-int tile_override() {
+}  // namespace
+
+int gemm_tile_override() {
   const char* e = getenv("TFD_GEMM_TILE");
   return e ? atoi(e) : 0;
 }
-
-}  // namespace
 
 // Vector (16-byte) loads are legal when every row start of both operands is
 // 16-byte aligned and each operand's contiguous extent is whole chunks.
@@ -382,7 +382,7 @@ bool gemm_vector_ok(const GemmDesc& d, int elem_bytes) {
 }
 
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s) {
-  const int tile = tile_override();
+  const int tile = gemm_tile_override();
   if (tile == 0 && gemm_bf16_256_ok(d)) return launch_gemm_bf16_256(d, s);
   if (!d.in_bf16 && (tile == 8 || (tile == 0 && gemm_small_preferred(d)))) return launch_gemm_small_f32(d, s);
   if (d.in_bf16) {

@@ -51,6 +51,9 @@ struct Params {
   int m, n, k;
   int epi;
   int tiles_m, tiles_n;
+  const uint16_t* features;  // ReluGrad epilogue: the stored forward output
+  int64_t ldf;
+  float* col_partial;        // [tiles_m][n] column sums of the stored tiles
 };
 
 __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
@@ -94,6 +97,13 @@ __device__ __forceinline__ void copy_tile(const bf16* X, int64_t ld, int mn0, in
   }
 }
 
+// Byte offset of element (row, col) of the 256 x 256 16-bit output tile
+// staged in LDS: 512-byte rows of 32 chunks of 16 bytes; chunk c of row r
+// sits at slot c ^ (4 * ((r >> 2) & 7)).
+__device__ __forceinline__ int epi_off(int row, int col) {
+  return row * 512 + (((col >> 3) ^ (((row >> 2) & 7) << 2)) << 4) + (col & 7) * 2;
+}
+
 // Fragment of 32 rows (A) or 32 columns (B) starting at `base`, k-step q.
 template <bool KC>
 __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, int lane) {
@@ -131,7 +141,11 @@ __device__ __forceinline__ void interleave_mfma_reads() {
   }
 }
 
-template <bool A_KC, bool B_KC, typename OutT, int kWavesM, int kWavesN>
+// RG: ReluGrad epilogue (16-bit output): the stored value is the rounded
+// product where the matching feature is > 0 and +0 elsewhere, and the tile's
+// column sums of the stored values go to col_partial (the first pass of
+// BiasAddGrad; fixed order: lanes, then the two half-waves, then waves).
+template <bool A_KC, bool B_KC, typename OutT, int kWavesM, int kWavesN, bool RG = false>
 __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p) {
   constexpr int kThreads = 64 * kWavesM * kWavesN;
   constexpr int kFM = kBM / kWavesM / 32, kFN = kBN / kWavesN / 32;  // fragments per wave
@@ -204,20 +218,85 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     }
   }
 
-  OutT* C = static_cast<OutT*>(p.c);
   const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
+  const int op = p.epi & kEpiOpMask;
+  if constexpr (sizeof(OutT) == 2) {
+    // 16-bit output: the rounded tile goes through LDS (row-major, 16-byte
+    // chunks XOR-swizzled so that both the fragment-layout writes and the
+    // row-chunk reads are free of bank conflicts), then leaves in coalesced
+    // 16-byte row chunks. The k loop's last barrier has passed, but waves may
+    // still be reading their last fragments: wait for all of them first.
+    __syncthreads();
+    char* tile = smem;  // 256 rows x 512 bytes
 #pragma unroll
-  for (int j = 0; j < kFN; ++j) {
-    const int col = n0 + wn * kWTN + j * 32 + l32;
-    const float bv = (p.epi & kEpiOpMask) != 0 ? p.bias[col] : 0.0f;
+    for (int j = 0; j < kFN; ++j) {
+      const int col = wn * kWTN + j * 32 + l32;
+      const float bv = op != 0 ? p.bias[n0 + col] : 0.0f;
 #pragma unroll
-    for (int i = 0; i < kFM; ++i) {
+      for (int i = 0; i < kFM; ++i) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        float v = acc[i][j][r] + bv;
-        if ((p.epi & kEpiOpMask) == 2) v = relu_f32(v);
-        store_from_f32(C + (int64_t)row * p.ldc + col, v, trunc16);
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          float v = acc[i][j][r] + bv;
+          if (op == 2) v = relu_f32(v);
+          *reinterpret_cast<uint16_t*>(tile + epi_off(row, col)) = bf16_bits_mode(v, trunc16);
+        }
+      }
+    }
+    __syncthreads();
+    constexpr int kRowStep = kThreads / 32;
+    const int cc = tid & 31;  // 16-byte chunk of the row: columns 8cc .. 8cc+7
+    float cs[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
+    for (int row = tid >> 5; row < kBM; row += kRowStep) {
+      u32x4 v = *reinterpret_cast<const u32x4*>(tile + epi_off(row, 8 * cc));
+      if constexpr (RG) {
+        // ReluGrad: keep the value where the stored feature is > 0, +0
+        // elsewhere; sum the kept values per column
+        const u32x4 f = *reinterpret_cast<const u32x4*>(p.features + (int64_t)(m0 + row) * p.ldf + n0 + 8 * cc);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = bf16_bits_to_f32(f[e] & 0xFFFFu) > 0.0f ? (v[e] & 0xFFFFu) : 0u;
+          const uint32_t hi = bf16_bits_to_f32(f[e] >> 16) > 0.0f ? (v[e] & 0xFFFF0000u) : 0u;
+          v[e] = lo | hi;
+          cs[2 * e] += bf16_bits_to_f32(lo);
+          cs[2 * e + 1] += bf16_bits_to_f32(hi >> 16);
+        }
+      }
+      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc) = v;
+    }
+    if constexpr (RG) {
+      // column sums: each thread's rows, then the kRowStep threads of a
+      // chunk in row-group order (a fixed order)
+      __syncthreads();
+      float* red = reinterpret_cast<float*>(smem);  // [kRowStep][256]
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[(tid >> 5) * kBN + 8 * cc + e] = cs[e];
+      __syncthreads();
+      for (int c = tid; c < kBN; c += kThreads) {
+        float t = 0.0f;
+#pragma unroll
+        for (int g = 0; g < kRowStep; ++g) t += red[g * kBN + c];
+        p.col_partial[(int64_t)tm * p.n + n0 + c] = t;
+      }
+    }
+    return;
+  } else {
+    OutT* C = static_cast<OutT*>(p.c);
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) {
+      const int col = n0 + wn * kWTN + j * 32 + l32;
+      const float bv = op != 0 ? p.bias[col] : 0.0f;
+#pragma unroll
+      for (int i = 0; i < kFM; ++i) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          float v = acc[i][j][r] + bv;
+          if (op == 2) v = relu_f32(v);
+          C[(int64_t)row * p.ldc + col] = v;
+        }
       }
     }
   }
@@ -239,8 +318,13 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.epi = d.epi;
   p.tiles_m = p.m / kBM;
   p.tiles_n = p.n / kBN;
+  p.features = static_cast<const uint16_t*>(d.features);
+  p.ldf = d.ldf;
+  p.col_partial = d.col_partial;
   dim3 grid(p.tiles_m * p.tiles_n), block(64 * WM * WN);
-  if (d.out_bf16)
+  if (d.features)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, true>), grid, block, 0, s, p);
+  else if (d.out_bf16)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN>), grid, block, 0, s, p);
   else
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float, WM, WN>), grid, block, 0, s, p);
@@ -268,8 +352,12 @@ int waves_for(const char* layout, int dflt) {
 }  // namespace
 
 bool gemm_bf16_256_ok(const GemmDesc& d) {
+  // a 16-bit C leaves in 16-byte row chunks (and so do ReluGrad features in)
+  auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  const bool c_ok = !d.out_bf16 || (al(d.c) && d.ldc % 8 == 0);
+  const bool f_ok = !d.features || (al(d.features) && d.ldf % 8 == 0);
   return d.in_bf16 && d.m % kBM == 0 && d.n % kBN == 0 && d.k % kBK == 0 && d.k > 0 &&
-         gemm_vector_ok(d, 2) && !(d.ta && d.tb);
+         gemm_vector_ok(d, 2) && !(d.ta && d.tb) && c_ok && f_ok;
 }
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {

@@ -21,6 +21,12 @@ struct GemmDesc {
   bool in_bf16, out_bf16;
   const float* bias;
   int epi;  // (epi & kEpiOpMask): 0 none, 1 bias, 2 bias + relu; kEpiTrunc16: truncating 16-bit output
+  // ReluGrad epilogue (16-bit whole-tile kernel only): when features != NULL
+  // the stored output is features > 0 ? C : +0, and each workgroup writes the
+  // column sums of its stored tile to col_partial[tile_row * n + col].
+  const void* features = nullptr;
+  int64_t ldf = 0;
+  float* col_partial = nullptr;
 };
 
 constexpr int kEpiOpMask = 3;
@@ -28,6 +34,8 @@ constexpr int kEpiTrunc16 = 16;
 
 bool gemm_vector_ok(const GemmDesc& d, int elem_bytes);
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s);
+// The TFD_GEMM_TILE tuning override (0 when unset).
+int gemm_tile_override();
 // 16-bit operands, whole 256 x 256 tiles, k a multiple of 64 (gemm_bf16.hip).
 bool gemm_bf16_256_ok(const GemmDesc& d);
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s);
@@ -51,6 +59,9 @@ hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* ou
 size_t loss_ws_bytes(int64_t count, bool bf16);
 hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, double* loss,
                                int64_t count, bool bf16, void* ws, hipStream_t s);
+
+// Sums `chunks` row-chunk partials of each column in chunk order (reduce.hip).
+hipError_t launch_colsum_final(const float* partial, float* db, int64_t chunks, int64_t cols, hipStream_t s);
 
 size_t softmax_xent_ws_bytes(int64_t rows);
 hipError_t launch_softmax_xent(const void* logits, const int32_t* labels, void* grad, double* loss, int64_t rows,

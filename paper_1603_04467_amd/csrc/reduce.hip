@@ -224,6 +224,12 @@ hipError_t launch_t(const T* g, const T* f, T* out, float* db, int64_t rows, int
 
 }  // namespace
 
+hipError_t launch_colsum_final(const float* partial, float* db, int64_t chunks, int64_t cols, hipStream_t s) {
+  const unsigned g = (unsigned)((cols + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(colsum_final_kernel, g, kThreads, 0, s, partial, db, chunks, cols);
+  return hipGetLastError();
+}
+
 size_t reduction_ws_bytes(int64_t rows, int64_t cols, bool bf16_t) {
   const ReducePlan p = plan(rows, cols, bf16_t ? 8 : 4);
   return (size_t)(p.row_chunks * cols) * sizeof(float);

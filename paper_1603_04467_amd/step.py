@@ -35,11 +35,19 @@ def _to_device(a: np.ndarray, act: str, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a)).to(device)
 
 
-def op_graph(w: Workload):
+def fused_below(w: Workload, l: int, fuse: bool) -> bool:
+    """Whether layer l's input-gradient MatMul also applies the ReluGrad and
+    BiasAddGrad of layer l - 1 (one fused call instead of two)."""
+    return fuse and 1 <= l < w.layers and w.relus[l - 1]
+
+
+def op_graph(w: Workload, fuse: bool = True):
     """(name, reads, writes) of every op of one step of ``w``, in program
     order. Keys name buffers: h<l> activations (h0 = x), g the cost gradient,
     dy<l>/dx<l>/dw<l>/db<l> the gradients of layer l, W<l>/b<l> its Variables
-    (all copies of the weights), ws the shared reduction workspace."""
+    (all copies of the weights), ws the shared reduction workspace. With
+    ``fuse``, the input-gradient MatMul of a layer above a Relu layer also
+    produces that layer's dY and db (no separate relugrad op, no stored dX)."""
     L = w.layers
     ops = [(f"fwd{l + 1}", (f"h{l}", f"W{l}", f"b{l}"), (f"h{l + 1}",)) for l in range(L)]
     if w.cost != "upstream":
@@ -47,9 +55,13 @@ def op_graph(w: Workload):
     gkey = "g"
     for l in reversed(range(L)):
         dykey = f"dy{l}" if w.relus[l] else gkey
-        rg_writes = (f"dy{l}", f"db{l}", "ws") if w.relus[l] else (f"db{l}", "ws")
-        ops.append((f"relugrad{l + 1}", (gkey, f"h{l + 1}"), rg_writes))
-        ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}",)))
+        if not fused_below(w, l + 1, fuse):
+            rg_writes = (f"dy{l}", f"db{l}", "ws") if w.relus[l] else (f"db{l}", "ws")
+            ops.append((f"relugrad{l + 1}", (gkey, f"h{l + 1}"), rg_writes))
+        if fused_below(w, l, fuse):
+            ops.append((f"dx{l + 1}", (dykey, f"W{l}", f"h{l}"), (f"dy{l - 1}", f"db{l - 1}", "ws")))
+        else:
+            ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}",)))
         ops.append((f"dw{l + 1}", (f"h{l}", dykey), (f"dw{l}",)))
         if w.update:
             ops.append((f"sgd{l + 1}", (f"dw{l}", f"db{l}"), (f"W{l}", f"b{l}")))
@@ -60,8 +72,9 @@ def op_graph(w: Workload):
 class DenseStep:
     """Device state and launch sequence of one step of workload ``w``."""
 
-    def __init__(self, w: Workload, inputs: dict, device="cuda"):
+    def __init__(self, w: Workload, inputs: dict, device="cuda", fuse: bool = True):
         self.w = w
+        self.fuse = fuse
         self.device = torch.device(device)
         self.act = torch.bfloat16 if w.act == "bf16" else torch.float32
         dev = self.device
@@ -96,6 +109,7 @@ class DenseStep:
         need = [T.tfd_reduction_workspace_size(N, w.dims[l + 1], self.act) for l in range(L)]
         need.append(T.tfd_loss_workspace_size(N * w.dims[-1], self.act))
         need.append(T.tfd_softmax_xent_workspace_size(N))
+        need += [T.tfd_matmul_relu_grad_workspace_size(N, w.dims[l], self.act) for l in range(1, L)]
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
         if self.weights_t is not None:
@@ -162,7 +176,12 @@ class DenseStep:
                     T.tfd_bias_add_grad(grad, self.db[l], workspace=ws, stream=st)
 
             def dx(st):
-                T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding, stream=st)
+                if fused_below(w, l, self.fuse):
+                    T.tfd_matmul_relu_grad_bias_add_grad(dyl, self.weights[l], self.h[l], self.dy[l - 1], self.db[l - 1],
+                                                         transpose_b=True, rounding=w.rounding, workspace=ws,
+                                                         stream=st)
+                else:
+                    T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding, stream=st)
 
             def dw(st):
                 T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True, stream=st)
@@ -181,7 +200,7 @@ class DenseStep:
         for l in reversed(range(L)):
             backward(l, grad)
             grad = self.dx[l]
-        return [Node(name, launches[name], reads, writes) for name, reads, writes in op_graph(w)]
+        return [Node(name, launches[name], reads, writes) for name, reads, writes in op_graph(w, self.fuse)]
 
     def run(self, mark=None, stream=None):
         """Enqueue one step in program order on one stream (the current one

@@ -32,7 +32,8 @@ EPILOGUES = {"none": 0, "bias": 1, "bias_relu": 2}
 EXPORTS = (
     "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
     "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
-    "tfd_relu_grad_bias_add_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
+    "tfd_relu_grad_bias_add_grad", "tfd_matmul_relu_grad_workspace_size", "tfd_matmul_relu_grad_bias_add_grad",
+    "tfd_loss_workspace_size", "tfd_l2_loss_grad",
     "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent",
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
 )
@@ -68,6 +69,9 @@ def load() -> ctypes.CDLL:
         "tfd_reduction_workspace_size": ([i64, i64, i32], sz),
         "tfd_bias_add_grad": ([vp, vp, i64, i64, i32, vp, sz, vp], i32),
         "tfd_relu_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
+        "tfd_matmul_relu_grad_workspace_size": ([i64, i64, i32], sz),
+        "tfd_matmul_relu_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32, vp,
+                                                sz, vp], i32),
         "tfd_loss_workspace_size": ([i64, i32], sz),
         "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
         "tfd_softmax_xent_workspace_size": ([i64], sz),
@@ -111,6 +115,8 @@ def _rowmajor(t: torch.Tensor, name: str) -> int:
     """Leading dimension of a 2-D row-major tensor (unit column stride)."""
     if t.dim() != 2:
         raise ValueError(f"{name} must be 2-D")
+    if t.numel() == 0:          # an empty matrix: strides carry no meaning
+        return max(t.size(1), 1)
     if t.stride(1) != 1 and t.size(1) > 1:
         raise ValueError(f"{name} must have unit column stride")
     return max(t.stride(0), t.size(1), 1)
@@ -168,6 +174,37 @@ def tfd_relu_grad(gradients, features, backprops, stream=None):
 
 def tfd_reduction_workspace_size(rows, cols, dtype) -> int:
     return load().tfd_reduction_workspace_size(rows, cols, TFD_BF16 if dtype == torch.bfloat16 else TFD_F32)
+
+
+def tfd_matmul_relu_grad_workspace_size(m, n, dtype) -> int:
+    return load().tfd_matmul_relu_grad_workspace_size(m, n, TFD_BF16 if dtype == torch.bfloat16 else TFD_F32)
+
+
+def tfd_matmul_relu_grad_bias_add_grad(a, b, features, backprops, bias_grad, transpose_a=False, transpose_b=False,
+                                       rounding="nearest", workspace=None, stream=None):
+    """backprops = ReluGrad(op(a) @ op(b), features), bias_grad = its column
+    sums (the input-gradient MatMul fused with the lower layer's ReluGrad and
+    BiasAddGrad; see include/tfdense.h)."""
+    lda, ldb = _rowmajor(a, "a"), _rowmajor(b, "b")
+    m = a.size(1) if transpose_a else a.size(0)
+    k = a.size(0) if transpose_a else a.size(1)
+    kb = b.size(1) if transpose_b else b.size(0)
+    n = b.size(0) if transpose_b else b.size(1)
+    if kb != k or tuple(backprops.shape) != (m, n) or tuple(features.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    for t, name in ((features, "features"), (backprops, "backprops")):
+        if not t.is_contiguous() or t.dtype != a.dtype:
+            raise ValueError(f"{name} must be contiguous with the operands' dtype")
+    if b.dtype != a.dtype:
+        raise ValueError("a and b must have the same dtype")
+    if bias_grad.dtype != torch.float32 or bias_grad.numel() != n or not bias_grad.is_contiguous():
+        raise ValueError("bias_grad must be a contiguous fp32 vector of length n")
+    ws = _workspace(tfd_matmul_relu_grad_workspace_size(m, n, a.dtype), a.device, workspace)
+    _check(load().tfd_matmul_relu_grad_bias_add_grad(int(transpose_a), int(transpose_b), m, n, k, _ptr(a), lda,
+                                                     _ptr(b), ldb, _ptr(features), _ptr(backprops), _ptr(bias_grad),
+                                                     _dtype(a), ROUNDINGS[rounding], _ptr(ws), ws.numel(),
+                                                     _stream(stream)))
+    return backprops, bias_grad
 
 
 def tfd_loss_workspace_size(count, dtype) -> int:

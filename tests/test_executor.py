@@ -7,7 +7,7 @@ import itertools
 import pytest
 
 from paper_1603_04467_amd import executor, workloads
-from paper_1603_04467_amd.step import op_graph
+from paper_1603_04467_amd.step import fused_below, op_graph
 
 
 class _N:
@@ -49,30 +49,38 @@ def test_schedule_is_topological_and_complete():
     assert len({plan[1], plan[2], plan[4]}) == 3      # three independent successors of node 0
 
 
+@pytest.mark.parametrize("fuse", [False, True])
 @pytest.mark.parametrize("name", sorted(workloads.WORKLOADS))
-def test_step_graph_orders_updates_after_reads(name):
+def test_step_graph_orders_updates_after_reads(name, fuse):
     w = workloads.workload(name)
-    ops = op_graph(w)
+    ops = op_graph(w, fuse)
     names = [o[0] for o in ops]
     deps = executor.transitive_reduction(executor.dependencies([_N(*o) for o in ops]))
     anc = _ancestors(deps)
     idx = {n: i for i, n in enumerate(names)}
     L = w.layers
+
+    def dy_producer(l):   # the op that writes layer l's masked gradient and db
+        return f"dx{l + 1}" if fused_below(w, l, fuse) else f"relugrad{l}"
+
     for l in range(1, L + 1):
         if w.update:
             s = idx[f"sgd{l}"]
             # the update of W_l and b_l waits for every reader of the old values
-            for r in (f"fwd{l}", f"dx{l}", f"dw{l}", f"relugrad{l}"):
+            for r in (f"fwd{l}", f"dx{l}", f"dw{l}", dy_producer(l)):
                 assert idx[r] in anc[s], (r, f"sgd{l}")
         # dX_l and dW_l are independent of each other (concurrent)
         dx, dw = idx[f"dx{l}"], idx[f"dw{l}"]
         assert dx not in anc[dw] and dw not in anc[dx]
         # both need the masked gradient, which needs the gradient from above
-        assert idx[f"relugrad{l}"] in anc[dx] or not w.relus[l - 1]
-        if l < L:
+        if w.relus[l - 1]:
+            assert idx[dy_producer(l)] in anc[dx] and idx[dy_producer(l)] in anc[dw]
+        if l < L and not fused_below(w, l, fuse):
             assert idx[f"dx{l + 1}"] in anc[idx[f"relugrad{l}"]]
+    # fused: one op per layer above a Relu layer replaces the relugrad op
+    assert ("relugrad1" in names) == (not fused_below(w, 1, fuse))
     # the forward chain precedes the cost and all of the backward pass
-    first_bwd = idx[f"relugrad{L}"]
+    first_bwd = min(i for i, n in enumerate(names) if not n.startswith("fwd") and n != "loss")
     assert idx[f"fwd{L}"] in anc[first_bwd]
     plan = dict(executor.schedule(deps, 3))
     for l in range(1, L + 1):

@@ -344,3 +344,48 @@ def test_relu_grad_bias_add_grad(dt, rows, cols, mask):
         T.tfd_bias_add_grad(g, db2)
     torch.cuda.synchronize()
     assert torch.equal(db, db2)
+
+
+# ------------------------------------- fused input gradient + ReluGrad + BiasAddGrad
+
+@pytest.mark.parametrize("m,n,k,layout,dt,rounding", [
+    (512, 768, 512, "NT", "bf16", "nearest"),     # whole 256 tiles: the fused epilogue
+    (1024, 512, 768, "NN", "bf16", "nearest"),
+    (512, 256, 1024, "TN", "bf16", "nearest"),
+    (512, 768, 512, "NT", "bf16", "truncate"),
+    (300, 200, 136, "NT", "bf16", "nearest"),     # ragged: MatMul, then ReluGrad in place
+    (256, 1024, 1024, "NT", "f32", "nearest"),    # fp32 small-problem path
+    (1024, 512, 256, "NT", "f32", "nearest"),
+    (0, 64, 32, "NT", "f32", "nearest"),          # no rows: bias_grad = 0
+])
+def test_matmul_relu_grad_bias_add_grad(m, n, k, layout, dt, rounding):
+    rng = np.random.default_rng([m, n, k, len(layout), dt == "bf16", rounding == "truncate"])
+    ta, tb = layout == "TN", layout == "NT"
+    a_h, a = _host(rng, (k, m) if ta else (m, k), dt)
+    b_h, b = _host(rng, (n, k) if tb else (k, n), dt)
+    f_h, f = _host(rng, (m, n), dt)
+    bp = _empty((m, n), dt)
+    db = torch.full((n,), float("nan"), device=DEV)
+    T.tfd_matmul_relu_grad_bias_add_grad(a, b, f, bp, db, transpose_a=ta, transpose_b=tb, rounding=rounding)
+    # the two calls it replaces
+    g = _empty((m, n), dt)
+    T.tfd_matmul(a, b, g, transpose_a=ta, transpose_b=tb, rounding=rounding)
+    bp2 = _empty((m, n), dt)
+    db2 = torch.full((n,), float("nan"), device=DEV)
+    T.tfd_relu_grad_bias_add_grad(g, f, bp2, db2)
+    torch.cuda.synchronize()
+    assert torch.equal(bp, bp2), "backprops differ from MatMul + ReluGrad"
+    dy = to_f64(bp2)
+    D = max(m, 1) * max(amax(dy), 1e-30)
+    assert_close(to_f64(db), oracle.bias_add_grad(dy), D, TAU["f32"], "fused BiasAddGrad")
+    # against the oracle's chain (mask decisions are exact here: features are given)
+    store = "bf16t" if rounding == "truncate" else dt
+    want = oracle.relu_grad(oracle.matmul(a_h, b_h, ta, tb, out=store), f_h)
+    Dg = k * amax(a_h) * amax(b_h)
+    assert_close(dy, want, Dg, TAU[dt], "fused dY")
+    # fixed summation order: a second call gives the same bits
+    db3 = torch.empty_like(db)
+    T.tfd_matmul_relu_grad_bias_add_grad(a, b, f, torch.empty_like(bp), db3, transpose_a=ta, transpose_b=tb,
+                                         rounding=rounding)
+    torch.cuda.synchronize()
+    assert torch.equal(db, db3)

@@ -24,7 +24,7 @@ import torch
 
 import oracle
 from paper_1603_04467_amd import workloads
-from paper_1603_04467_amd.step import DenseStep
+from paper_1603_04467_amd.step import DenseStep, fused_below
 from tests.parity import TAU, amax, assert_bits, assert_close, to_f64
 
 pytestmark = pytest.mark.gpu
@@ -62,8 +62,8 @@ def _assert_within(got, want, allowed, what):
     assert e <= allowed, f"{what}: max|err| = {e:.3e} > allowed {allowed:.3e}"
 
 
-def _run_gpu(w, inp):
-    s = DenseStep(w, inp)
+def _run_gpu(w, inp, fuse=True):
+    s = DenseStep(w, inp, fuse=fuse)
     s.run()
     torch.cuda.synchronize()
     return s
@@ -88,8 +88,9 @@ def _check_mask_consistency(s, l):
 
 
 def _check_adjoint(s, l, tau):
-    """<G_l, H_l> = <W_l, dW_l> + <b_l, db_l> on the GPU's tensors."""
-    g = to_f64(s.g if l == s.w.layers - 1 else s.dx[l + 1])
+    """<G_l, H_l> = <W_l, dW_l> + <b_l, db_l> on the GPU's tensors (with
+    <dY_l, H_l> for <G_l, H_l>: the mask only zeroes entries where H_l = 0)."""
+    g = to_f64(s.dy_of(l))
     h = to_f64(s.h[l + 1])
     x = to_f64(s.h[l])
     dy = to_f64(s.dy_of(l))
@@ -157,13 +158,15 @@ def _compare_full(w, inp, s):
         dy_ref = ref["dy"][l]
         dy_gpu = to_f64(s.dy_of(l))
         if w.relus[l]:
-            _check_mask_consistency(s, l)
+            if not fused_below(w, l + 1, s.fuse):
+                _check_mask_consistency(s, l)
             assert_close(dy_gpu[keep], dy_ref[keep], D_g, tau, f"dY_{l + 1}")
         W = hi["weights"][l]
         M = w.dims[l + 1]
         md = amax(dy_ref)
         D_dx = M * md * amax(W)
-        assert_close(to_f64(s.dx[l])[keep], ref["dx"][l][keep], D_dx, tau, f"dX_{l + 1}")
+        if not fused_below(w, l, s.fuse):     # fused: dX_l is not stored, only the dY below it
+            assert_close(to_f64(s.dx[l])[keep], ref["dx"][l][keep], D_dx, tau, f"dX_{l + 1}")
         mh = amax(ref["h"][l])
         _assert_within(to_f64(s.dw[l]), ref["dw"][l], tau * w.batch * mh * md + 2 * nt * mh * md, f"dW_{l + 1}")
         _assert_within(to_f64(s.db[l]), ref["db"][l], tau * w.batch * md + 2 * nt * md, f"db_{l + 1}")
@@ -208,15 +211,44 @@ SCALED = [
 ]
 
 
+@pytest.mark.parametrize("fuse", [True, False])
 @pytest.mark.parametrize("name,batch,dims", SCALED)
-def test_step_matches_oracle(name, batch, dims):
+def test_step_matches_oracle(name, batch, dims, fuse):
     w = workloads.workload(name)
     if batch is not None:
         w = w.scaled(batch=batch, dims=dims)
     inp = workloads.generate(w, seed=0)
-    s = _run_gpu(w, inp)
+    s = _run_gpu(w, inp, fuse=fuse)
     flips = _compare_full(w, inp, s)
     print(f"{w.name}: {flips} rows with in-band Relu mask differences")
+
+
+@pytest.mark.parametrize("name,batch,dims", [("mlp784-1024-1024-10", None, None),
+                                             ("wide4096x4-bf16", 1032, (512, 768, 512, 256, 512)),
+                                             ("wide4096x4-bf16-trunc", 600, (256, 384, 264, 128, 200)),
+                                             ("wide4096x4-f32", 520, (136, 256, 512, 264, 128))])
+def test_fused_step_equals_unfused(name, batch, dims):
+    """The fused input-gradient/ReluGrad/BiasAddGrad call stores the same dY
+    bits as the two calls it replaces, so every tensor downstream of dY is
+    bitwise equal; only db (and the bias update) may differ, by the order of
+    the column sums."""
+    w = workloads.workload(name)
+    if batch is not None:
+        w = w.scaled(batch=batch, dims=dims)
+    inp = workloads.generate(w, seed=5)
+    a = _run_gpu(w, inp, fuse=True)
+    b = _run_gpu(w, inp, fuse=False)
+    for l in range(w.layers):
+        assert torch.equal(a.h[l + 1], b.h[l + 1])
+        assert torch.equal(a.dy_of(l), b.dy_of(l)), f"dY_{l + 1}"
+        assert torch.equal(a.dw[l], b.dw[l]), f"dW_{l + 1}"
+        assert torch.equal(a.weights[l], b.weights[l]), f"W_{l + 1}"
+        md = float(b.dy_of(l).abs().max())
+        tol = TAU["f32"] * w.batch * md
+        assert float((a.db[l] - b.db[l]).abs().max()) <= tol, f"db_{l + 1}"
+        assert float((a.biases[l] - b.biases[l]).abs().max()) <= w.lr * tol + 2.0 ** -23 * float(
+            b.biases[l].abs().max()), f"b_{l + 1}"
+    assert torch.equal(a.dx[0], b.dx[0])
 
 
 @pytest.mark.parametrize("name", ["dense784x100", "mlp784-1024-1024-10-xent", "wide4096x4-bf16"])
@@ -226,14 +258,15 @@ def test_step_is_deterministic(name):
         w = w.scaled(batch=1032, dims=(512, 768, 512, 256, 512))
     inp = workloads.generate(w, seed=3)
     s = DenseStep(w, inp)
+    dx = [s.dx[l] for l in range(w.layers) if not fused_below(w, l, s.fuse)]
     s.run()
-    first = [t.clone() for t in s.dx + s.dw + s.db + s.variables()] + [s.loss.clone()]
+    first = [t.clone() for t in dx + s.dw + s.db + s.variables()] + [s.loss.clone()]
     s.restore()
     s.run()
     torch.cuda.synchronize()
-    second = [t for t in s.dx + s.dw + s.db + s.variables()] + [s.loss]
+    second = [t for t in dx + s.dw + s.db + s.variables()] + [s.loss]
     for a, b in zip(first, second):
-        assert torch.equal(a, b)
+        assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
 
 
 # ---------------------------------------------------------------- full sizes
@@ -283,7 +316,8 @@ def _check_full_size(name):
     md = amax(g_ref)
     mh = amax(h_ref[top])
     dx_top = oracle.matmul(g_ref, hi["weights"][top], transpose_b=True, out=_store(w))
-    assert_close(to_f64(s.dx[top]), dx_top, w.dims[-1] * md * amax(hi["weights"][top]), tau, f"dX_{L}")
+    if not fused_below(w, top, s.fuse):
+        assert_close(to_f64(s.dx[top]), dx_top, w.dims[-1] * md * amax(hi["weights"][top]), tau, f"dX_{L}")
     assert_close(to_f64(s.dw[top]), oracle.matmul(h_ref[top], g_ref, transpose_a=True, out="f32"),
                  w.batch * mh * md, tau, f"dW_{L}")
     assert_close(to_f64(s.db[top]), oracle.bias_add_grad(g_ref), w.batch * md, tau, f"db_{L}")
@@ -297,10 +331,11 @@ def _check_full_size(name):
         assert_close(to_f64(s.dy[l])[rows], dy_rows, D_g, tau, f"dY_{l + 1} (sampled rows)")
         dx_rows = oracle.matmul(dy_rows, hi["weights"][l], transpose_b=True, out=_store(w))
         D_dx = w.dims[l + 1] * amax(dy_rows) * amax(hi["weights"][l])
-        assert_close(to_f64(s.dx[l])[rows], dx_rows, D_dx, tau, f"dX_{l + 1} (sampled rows)")
+        if not fused_below(w, l, s.fuse):
+            assert_close(to_f64(s.dx[l])[rows], dx_rows, D_dx, tau, f"dX_{l + 1} (sampled rows)")
         g_rows, D_g = dx_rows, D_dx
     for l in range(L):
-        if w.relus[l]:
+        if w.relus[l] and not fused_below(w, l + 1, s.fuse):
             _check_mask_consistency(s, l)
         _check_adjoint(s, l, tau)
     return int(touched.sum())
