@@ -127,3 +127,25 @@ def test_softmax_and_conversion_validation(lib):
     assert lib.tfd_apply_gradient_descent(FAKE, ctypes.c_float(0.01), FAKE * 2, 100, None, 5, None) == 1
     assert lib.tfd_apply_gradient_descent_matrix(FAKE, ctypes.c_float(0.01), FAKE * 2, 10, 10, None, None, 5,
                                                  None) == 1
+
+
+def test_fused_relu_grad_matmul_validation(lib):
+    f = lib.tfd_matmul_relu_grad_bias_add_grad
+    need = lib.tfd_matmul_relu_grad_workspace_size(512, 256, 1)
+    assert need >= 2 * 256 * 4
+    args = dict(a=FAKE, b=FAKE * 2, feat=FAKE * 3, bp=FAKE * 4, db=FAKE * 5, ws=FAKE * 6)
+
+    def call(ta=0, tb=1, m=512, n=256, k=128, lda=128, ldb=128, dtype=1, rounding=0, ws=args["ws"], ws_bytes=need,
+             bp=args["bp"], feat=args["feat"], db=args["db"]):
+        return f(ta, tb, m, n, k, args["a"], lda, args["b"], ldb, feat, bp, db, dtype, rounding, ws, ws_bytes, None)
+
+    assert call(m=-1) == 1
+    assert call(ta=1, tb=1) == 2
+    assert call(lda=64) == 1 and b"leading dimension" in lib.tfd_last_error()
+    assert call(ws_bytes=need - 1) == 1 and b"workspace" in lib.tfd_last_error()
+    assert call(db=None) == 1
+    assert call(feat=None) == 1
+    assert call(dtype=0, rounding=1) == 1 and b"16-bit" in lib.tfd_last_error()
+    assert call(rounding=9) == 1
+    assert call(bp=args["feat"] + 64) == 1 and b"overlap" in lib.tfd_last_error()
+    assert call(n=0, feat=None, bp=None, db=None, ws=None, ws_bytes=0) == 0      # nothing to do
