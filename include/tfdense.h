@@ -202,6 +202,31 @@ TFD_API tfd_status tfd_l2_loss_grad(const void* output, const void* target, void
                             int64_t count, tfd_dtype type,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/* Workspace bytes that tfd_matmul_l2_loss_grad needs for an m x n output. */
+TFD_API size_t tfd_matmul_l2_loss_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type);
+
+/*
+ * The output layer's MatMul fused with the squared-error cost head and the
+ * output layer's BiasAddGrad (Figure 1's MatMul and Add on the last layer,
+ * then section 4.1's first gradient ops):
+ *   output[r, c]    = (op(A) op(B))[r, c] + bias[c], fp32 accumulation, rounded
+ *                     once to `type` (with `rounding` for 16-bit outputs),
+ *   grad[r, c]      = output[r, c] - target[r, c], as tfd_l2_loss_grad computes it,
+ *   loss            = 1/2 sum grad_exact^2 (float64, fixed order),
+ *   bias_grad[c]    = sum_r grad[r, c] (fp32, fixed order).
+ * Operands as in tfd_matmul; output, target and grad are m x n of `type`,
+ * contiguous (ld = n); bias is fp32[n]; target == NULL means 0 (as in
+ * tfd_l2_loss_grad). output and grad equal what
+ * tfd_matmul, tfd_l2_loss_grad and tfd_bias_add_grad store, bit for bit;
+ * loss and bias_grad may differ from that path in the order of their sums.
+ * No output buffer may overlap an input or another output.
+ */
+TFD_API tfd_status tfd_matmul_l2_loss_grad(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                   const void* a, int64_t lda, const void* b, int64_t ldb, const float* bias,
+                                   void* output, const void* target, void* grad, double* loss,
+                                   float* bias_grad, tfd_dtype type, tfd_rounding rounding,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace bytes that tfd_softmax_cross_entropy_grad needs for `rows` rows. */
 TFD_API size_t tfd_softmax_xent_workspace_size(int64_t rows);
 

@@ -280,6 +280,102 @@ tfd_status tfd_matmul_relu_grad_bias_add_grad(int transpose_a, int transpose_b, 
                     "tfd_matmul_relu_grad_bias_add_grad launch");
 }
 
+size_t tfd_matmul_l2_loss_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type) {
+  if (m < 0 || n < 0 || !valid_dtype(type)) return 0;
+  const bool h = type == TFD_BF16;
+  const int64_t tiles = ((m + 255) / 256) * ((n + 255) / 256);
+  const size_t fused = (size_t)((m + 255) / 256) * (size_t)n * sizeof(float) + (size_t)tiles * sizeof(double);
+  size_t plain = tfd::loss_ws_bytes(m * n, h);
+  const size_t red = tfd::reduction_ws_bytes(m, n, h);
+  if (red > plain) plain = red;
+  return fused > plain ? fused : plain;
+}
+
+tfd_status tfd_matmul_l2_loss_grad(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k, const void* a,
+                                   int64_t lda, const void* b, int64_t ldb, const float* bias, void* output,
+                                   const void* target, void* grad, double* loss, float* bias_grad, tfd_dtype type,
+                                   tfd_rounding rounding, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_matmul_l2_loss_grad";
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "%s: unknown rounding", fn);
+  if (rounding == TFD_ROUND_TRUNCATE && type != TFD_BF16)
+    return fail(TFD_EINVAL, "%s: truncation needs a 16-bit output", fn);
+  if (transpose_a && transpose_b) return fail(TFD_EUNSUPPORTED, "%s: transpose_a and transpose_b together", fn);
+  if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30))
+    return fail(TFD_EUNSUPPORTED, "%s: dimension above 2^30", fn);
+  const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
+  const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
+  if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1))
+    return fail(TFD_EINVAL, "%s: leading dimension smaller than the row", fn);
+  if (!loss) return fail(TFD_EINVAL, "%s: loss is NULL", fn);
+  if (n > 0 && (!bias || !bias_grad)) return fail(TFD_EINVAL, "%s: NULL bias or bias_grad", fn);
+  const size_t need = tfd_matmul_l2_loss_grad_workspace_size(m, n, type);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need, workspace_bytes);
+  if (m > 0 && n > 0 && (!output || !grad || (k > 0 && (!a || !b))))
+    return fail(TFD_EINVAL, "%s: NULL pointer", fn);
+  const int eb = elem_bytes(type);
+  const size_t cs = (size_t)m * (size_t)n * eb, as = span(a_rows, a_cols, lda, eb), bs = span(b_rows, b_cols, ldb, eb);
+  const size_t nb = (size_t)n * 4;
+  const void* outs[] = {output, grad, bias_grad, loss, workspace};
+  const size_t out_sz[] = {cs, cs, nb, 8, need};
+  const void* ins[] = {a, b, bias, target};
+  const size_t in_sz[] = {as, bs, nb, cs};
+  for (int i = 0; i < 5; ++i) {
+    for (int j = 0; j < 4; ++j)
+      if (overlaps(outs[i], out_sz[i], ins[j], in_sz[j])) return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+    for (int j = i + 1; j < 5; ++j)
+      if (overlaps(outs[i], out_sz[i], outs[j], out_sz[j])) return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+  }
+  hipStream_t st = as_stream(stream);
+  if (n == 0)  // no columns: an empty sum
+    return hip_status(tfd::launch_loss_final(static_cast<const double*>(workspace), 0, loss, st),
+                      "tfd_matmul_l2_loss_grad launch");
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.a = a;
+  d.lda = lda;
+  d.b = b;
+  d.ldb = ldb;
+  d.c = output;
+  d.ldc = n;
+  d.in_bf16 = type == TFD_BF16;
+  d.out_bf16 = type == TFD_BF16;
+  d.bias = bias;
+  d.epi = TFD_EPI_BIAS | (rounding == TFD_ROUND_TRUNCATE ? tfd::kEpiTrunc16 : 0);
+  d.target = target;
+  d.grad = grad;
+  const int64_t tiles_m = (m + 255) / 256, tiles = tiles_m * ((n + 255) / 256);
+  d.col_partial = static_cast<float*>(workspace);
+  d.loss_partial = reinterpret_cast<double*>(static_cast<char*>(workspace) + (size_t)tiles_m * n * sizeof(float));
+  if (m > 0 && target && tfd::gemm_bf16_256_ok(d) && tfd::gemm_tile_override() == 0 &&
+      (reinterpret_cast<uintptr_t>(d.loss_partial) & 7) == 0 && tiles < (1LL << 31)) {
+    hipError_t e = tfd::launch_gemm_bf16_256(d, st);
+    if (e == hipSuccess) e = tfd::launch_colsum_final(d.col_partial, bias_grad, tiles_m, n, st);
+    if (e == hipSuccess) e = tfd::launch_loss_final(d.loss_partial, (int)tiles, loss, st);
+    return hip_status(e, "tfd_matmul_l2_loss_grad launch");
+  }
+  // other shapes: the three calls in sequence (they share the workspace in
+  // stream order)
+  d.target = nullptr;
+  d.grad = nullptr;
+  d.col_partial = nullptr;
+  d.loss_partial = nullptr;
+  hipError_t e = hipSuccess;
+  if (m > 0) e = tfd::launch_gemm(d, st);
+  if (e == hipSuccess)
+    e = tfd::launch_l2_loss_grad(output, target, grad, loss, m * n, type == TFD_BF16, workspace, st);
+  if (e == hipSuccess)
+    e = tfd::launch_relu_grad_bias_add_grad(grad, nullptr, nullptr, bias_grad, m, n, type == TFD_BF16, workspace, st);
+  return hip_status(e, "tfd_matmul_l2_loss_grad launch");
+}
+
 size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type) {
   if (count < 0 || !valid_dtype(type)) return 0;
   return tfd::loss_ws_bytes(count, type == TFD_BF16);

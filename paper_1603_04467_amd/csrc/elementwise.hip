@@ -393,6 +393,11 @@ hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, 
   return hipGetLastError();
 }
 
+hipError_t launch_loss_final(const double* partial, int n, double* loss, hipStream_t s) {
+  hipLaunchKernelGGL(loss_final_kernel, 1, kThreads, 0, s, partial, n, loss);
+  return hipGetLastError();
+}
+
 hipError_t launch_sgd(float* var, float alpha, const float* delta, int64_t count, uint16_t* shadow, bool trunc,
                       hipStream_t s) {
   const bool vec = aligned16(var) && aligned16(delta) && ((reinterpret_cast<uintptr_t>(shadow) & 7) == 0);

@@ -54,7 +54,13 @@ struct Params {
   const uint16_t* features;  // ReluGrad epilogue: the stored forward output
   int64_t ldf;
   float* col_partial;        // [tiles_m][n] column sums of the stored tiles
+  const uint16_t* target;    // squared-error epilogue: target and gradient (ld = n)
+  uint16_t* grad;
+  double* loss_partial;      // [tiles] float64 sums of squared differences
 };
+
+// Epilogues of the whole-tile kernel beyond bias/ReLU (16-bit outputs only).
+constexpr int kEpPlain = 0, kEpReluGrad = 1, kEpLoss = 2;
 
 __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int swz_mn(int krow) { return (krow & 3) << 2; }
@@ -141,11 +147,15 @@ __device__ __forceinline__ void interleave_mfma_reads() {
   }
 }
 
-// RG: ReluGrad epilogue (16-bit output): the stored value is the rounded
-// product where the matching feature is > 0 and +0 elsewhere, and the tile's
-// column sums of the stored values go to col_partial (the first pass of
-// BiasAddGrad; fixed order: lanes, then the two half-waves, then waves).
-template <bool A_KC, bool B_KC, typename OutT, int kWavesM, int kWavesN, bool RG = false>
+// EP (16-bit output only):
+//  kEpReluGrad: the stored value is the rounded product where the matching
+//    feature is > 0 and +0 elsewhere; the tile's column sums of the stored
+//    values go to col_partial (the first pass of BiasAddGrad);
+//  kEpLoss: the output is stored, and also grad = output - target (fp32
+//    difference, rounded to nearest even), the tile's float64 sum of squared
+//    differences (loss_partial) and its column sums of grad (col_partial).
+// Sums run in a fixed order: each thread's rows, then row groups in order.
+template <bool A_KC, bool B_KC, typename OutT, int kWavesM, int kWavesN, int EP = kEpPlain>
 __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p) {
   constexpr int kThreads = 64 * kWavesM * kWavesN;
   constexpr int kFM = kBM / kWavesM / 32, kFN = kBN / kWavesN / 32;  // fragments per wave
@@ -249,9 +259,27 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     float cs[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
+    double sq = 0.0;
     for (int row = tid >> 5; row < kBM; row += kRowStep) {
       u32x4 v = *reinterpret_cast<const u32x4*>(tile + epi_off(row, 8 * cc));
-      if constexpr (RG) {
+      const int64_t at = (int64_t)(m0 + row) * p.n + n0 + 8 * cc;  // contiguous side buffers
+      if constexpr (EP == kEpLoss) {
+        const u32x4 t = *reinterpret_cast<const u32x4*>(p.target + at);
+        u32x4 g;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d0 = bf16_bits_to_f32(v[e] & 0xFFFFu) - bf16_bits_to_f32(t[e] & 0xFFFFu);
+          const float d1 = bf16_bits_to_f32(v[e] >> 16) - bf16_bits_to_f32(t[e] >> 16);
+          sq += (double)d0 * (double)d0;
+          sq += (double)d1 * (double)d1;
+          const uint32_t g0 = bf16_bits(d0), g1 = bf16_bits(d1);
+          g[e] = g0 | (g1 << 16);
+          cs[2 * e] += bf16_bits_to_f32(g0);
+          cs[2 * e + 1] += bf16_bits_to_f32(g1);
+        }
+        *reinterpret_cast<u32x4*>(p.grad + at) = g;
+      }
+      if constexpr (EP == kEpReluGrad) {
         // ReluGrad: keep the value where the stored feature is > 0, +0
         // elsewhere; sum the kept values per column
         const u32x4 f = *reinterpret_cast<const u32x4*>(p.features + (int64_t)(m0 + row) * p.ldf + n0 + 8 * cc);
@@ -266,19 +294,36 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
       }
       *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc) = v;
     }
-    if constexpr (RG) {
+    if constexpr (EP != kEpPlain) {
       // column sums: each thread's rows, then the kRowStep threads of a
       // chunk in row-group order (a fixed order)
       __syncthreads();
       float* red = reinterpret_cast<float*>(smem);  // [kRowStep][256]
 #pragma unroll
       for (int e = 0; e < 8; ++e) red[(tid >> 5) * kBN + 8 * cc + e] = cs[e];
+      if constexpr (EP == kEpLoss) {
+        double* dred = reinterpret_cast<double*>(smem + kRowStep * kBN * 4);  // [kThreads]
+        dred[tid] = sq;
+      }
       __syncthreads();
       for (int c = tid; c < kBN; c += kThreads) {
         float t = 0.0f;
 #pragma unroll
         for (int g = 0; g < kRowStep; ++g) t += red[g * kBN + c];
         p.col_partial[(int64_t)tm * p.n + n0 + c] = t;
+      }
+      if constexpr (EP == kEpLoss) {
+        // wave 0: lane i adds dred[i], dred[i + 64], ... in order, then a
+        // butterfly over the 64 lanes (a fixed pattern)
+        if (wave == 0) {
+          const double* dred = reinterpret_cast<const double*>(smem + kRowStep * kBN * 4);
+          double t = 0.0;
+#pragma unroll
+          for (int i = 0; i < kThreads / 64; ++i) t += dred[lane + 64 * i];
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+          if (lane == 0) p.loss_partial[(int64_t)tm * p.tiles_n + tn] = t;
+        }
       }
     }
     return;
@@ -321,9 +366,14 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.features = static_cast<const uint16_t*>(d.features);
   p.ldf = d.ldf;
   p.col_partial = d.col_partial;
+  p.target = static_cast<const uint16_t*>(d.target);
+  p.grad = static_cast<uint16_t*>(d.grad);
+  p.loss_partial = d.loss_partial;
   dim3 grid(p.tiles_m * p.tiles_n), block(64 * WM * WN);
   if (d.features)
-    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, true>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpReluGrad>), grid, block, 0, s, p);
+  else if (d.target)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpLoss>), grid, block, 0, s, p);
   else if (d.out_bf16)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN>), grid, block, 0, s, p);
   else
@@ -356,8 +406,9 @@ bool gemm_bf16_256_ok(const GemmDesc& d) {
   auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
   const bool c_ok = !d.out_bf16 || (al(d.c) && d.ldc % 8 == 0);
   const bool f_ok = !d.features || (al(d.features) && d.ldf % 8 == 0);
+  const bool l_ok = !d.target || (al(d.target) && al(d.grad) && d.n % 8 == 0);
   return d.in_bf16 && d.m % kBM == 0 && d.n % kBN == 0 && d.k % kBK == 0 && d.k > 0 &&
-         gemm_vector_ok(d, 2) && !(d.ta && d.tb) && c_ok && f_ok;
+         gemm_vector_ok(d, 2) && !(d.ta && d.tb) && c_ok && f_ok && l_ok;
 }
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {

@@ -27,6 +27,13 @@ struct GemmDesc {
   const void* features = nullptr;
   int64_t ldf = 0;
   float* col_partial = nullptr;
+  // Squared-error epilogue (16-bit whole-tile kernel only): when target !=
+  // NULL, grad = C - target (contiguous, ld = n) is stored as well, each
+  // workgroup writes its tile's float64 sum of squared differences to
+  // loss_partial[tile] and the column sums of its grad tile to col_partial.
+  const void* target = nullptr;
+  void* grad = nullptr;
+  double* loss_partial = nullptr;
 };
 
 constexpr int kEpiOpMask = 3;
@@ -59,6 +66,8 @@ hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* ou
 size_t loss_ws_bytes(int64_t count, bool bf16);
 hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, double* loss,
                                int64_t count, bool bf16, void* ws, hipStream_t s);
+// loss = 1/2 * (sum of n float64 partials, fixed order) (elementwise.hip).
+hipError_t launch_loss_final(const double* partial, int n, double* loss, hipStream_t s);
 
 // Sums `chunks` row-chunk partials of each column in chunk order (reduce.hip).
 hipError_t launch_colsum_final(const float* partial, float* db, int64_t chunks, int64_t cols, hipStream_t s);

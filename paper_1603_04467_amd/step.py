@@ -41,6 +41,13 @@ def fused_below(w: Workload, l: int, fuse: bool) -> bool:
     return fuse and 1 <= l < w.layers and w.relus[l - 1]
 
 
+def fused_top(w: Workload, fuse: bool) -> bool:
+    """Whether the output layer's MatMul also computes the squared-error cost,
+    its gradient and the output layer's BiasAddGrad (one fused call instead
+    of three; only for an identity output layer)."""
+    return fuse and w.cost in ("sq_err", "half_sq") and not w.relus[-1]
+
+
 def op_graph(w: Workload, fuse: bool = True):
     """(name, reads, writes) of every op of one step of ``w``, in program
     order. Keys name buffers: h<l> activations (h0 = x), g the cost gradient,
@@ -50,12 +57,15 @@ def op_graph(w: Workload, fuse: bool = True):
     produces that layer's dY and db (no separate relugrad op, no stored dX)."""
     L = w.layers
     ops = [(f"fwd{l + 1}", (f"h{l}", f"W{l}", f"b{l}"), (f"h{l + 1}",)) for l in range(L)]
-    if w.cost != "upstream":
+    if fused_top(w, fuse):
+        ops[-1] = (f"fwd{L}", (f"h{L - 1}", f"W{L - 1}", f"b{L - 1}", "target"),
+                   (f"h{L}", "g", "loss", f"db{L - 1}", "ws"))
+    elif w.cost != "upstream":
         ops.append(("loss", (f"h{L}", "target"), ("g", "loss", "ws")))
     gkey = "g"
     for l in reversed(range(L)):
         dykey = f"dy{l}" if w.relus[l] else gkey
-        if not fused_below(w, l + 1, fuse):
+        if not fused_below(w, l + 1, fuse) and not (l == L - 1 and fused_top(w, fuse)):
             rg_writes = (f"dy{l}", f"db{l}", "ws") if w.relus[l] else (f"db{l}", "ws")
             ops.append((f"relugrad{l + 1}", (gkey, f"h{l + 1}"), rg_writes))
         if fused_below(w, l, fuse):
@@ -110,6 +120,7 @@ class DenseStep:
         need.append(T.tfd_loss_workspace_size(N * w.dims[-1], self.act))
         need.append(T.tfd_softmax_xent_workspace_size(N))
         need += [T.tfd_matmul_relu_grad_workspace_size(N, w.dims[l], self.act) for l in range(1, L)]
+        need.append(T.tfd_matmul_l2_loss_grad_workspace_size(N, w.dims[-1], self.act))
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
         if self.weights_t is not None:
@@ -158,6 +169,15 @@ class DenseStep:
 
         for l in range(L):
             launches[f"fwd{l + 1}"] = fwd(l)
+        if fused_top(w, self.fuse):
+            top = L - 1
+            src = self.weights_t[top] if self.weights_t is not None else self.weights[top]
+
+            def fwd_loss(st):
+                T.tfd_matmul_l2_loss_grad(self.h[top], src, self.biases[top], self.h[L], self.target, self.g,
+                                          self.loss, self.db[top], transpose_b=self.weights_t is not None,
+                                          rounding=w.rounding, workspace=ws, stream=st)
+            launches[f"fwd{L}"] = fwd_loss
 
         def loss(st):
             if self.labels is not None:

@@ -33,7 +33,7 @@ EXPORTS = (
     "tfd_abi_version", "tfd_status_string", "tfd_last_error", "tfd_matmul", "tfd_bias_add",
     "tfd_relu", "tfd_relu_grad", "tfd_reduction_workspace_size", "tfd_bias_add_grad",
     "tfd_relu_grad_bias_add_grad", "tfd_matmul_relu_grad_workspace_size", "tfd_matmul_relu_grad_bias_add_grad",
-    "tfd_loss_workspace_size", "tfd_l2_loss_grad",
+    "tfd_matmul_l2_loss_grad_workspace_size", "tfd_matmul_l2_loss_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
     "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent",
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
 )
@@ -72,6 +72,9 @@ def load() -> ctypes.CDLL:
         "tfd_matmul_relu_grad_workspace_size": ([i64, i64, i32], sz),
         "tfd_matmul_relu_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32, vp,
                                                 sz, vp], i32),
+        "tfd_matmul_l2_loss_grad_workspace_size": ([i64, i64, i32], sz),
+        "tfd_matmul_l2_loss_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, vp, vp, vp, i32, i32, vp, sz,
+                                     vp], i32),
         "tfd_loss_workspace_size": ([i64, i32], sz),
         "tfd_l2_loss_grad": ([vp, vp, vp, vp, i64, i32, vp, sz, vp], i32),
         "tfd_softmax_xent_workspace_size": ([i64], sz),
@@ -205,6 +208,40 @@ def tfd_matmul_relu_grad_bias_add_grad(a, b, features, backprops, bias_grad, tra
                                                      _dtype(a), ROUNDINGS[rounding], _ptr(ws), ws.numel(),
                                                      _stream(stream)))
     return backprops, bias_grad
+
+
+def tfd_matmul_l2_loss_grad_workspace_size(m, n, dtype) -> int:
+    return load().tfd_matmul_l2_loss_grad_workspace_size(m, n, TFD_BF16 if dtype == torch.bfloat16 else TFD_F32)
+
+
+def tfd_matmul_l2_loss_grad(a, b, bias, output, target, grad, loss, bias_grad, transpose_a=False, transpose_b=False,
+                            rounding="nearest", workspace=None, stream=None):
+    """output = op(a) @ op(b) + bias, grad = output - target, loss = 1/2 |grad|^2,
+    bias_grad = column sums of grad (the output layer fused with the
+    squared-error head and its BiasAddGrad; see include/tfdense.h)."""
+    lda, ldb = _rowmajor(a, "a"), _rowmajor(b, "b")
+    m = a.size(1) if transpose_a else a.size(0)
+    k = a.size(0) if transpose_a else a.size(1)
+    kb = b.size(1) if transpose_b else b.size(0)
+    n = b.size(0) if transpose_b else b.size(1)
+    if kb != k or tuple(output.shape) != (m, n) or tuple(grad.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    for t, name in ((output, "output"), (grad, "grad")) + (() if target is None else ((target, "target"),)):
+        if not t.is_contiguous() or t.dtype != a.dtype or tuple(t.shape) != (m, n):
+            raise ValueError(f"{name} must be a contiguous {m}x{n} matrix with the operands' dtype")
+    if b.dtype != a.dtype:
+        raise ValueError("a and b must have the same dtype")
+    for t, name in ((bias, "bias"), (bias_grad, "bias_grad")):
+        if t.dtype != torch.float32 or t.numel() != n or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 vector of length n")
+    if loss.dtype != torch.float64 or loss.numel() < 1:
+        raise ValueError("loss must be a float64 tensor")
+    ws = _workspace(tfd_matmul_l2_loss_grad_workspace_size(m, n, a.dtype), a.device, workspace)
+    _check(load().tfd_matmul_l2_loss_grad(int(transpose_a), int(transpose_b), m, n, k, _ptr(a), lda, _ptr(b), ldb,
+                                          _ptr(bias), _ptr(output), _ptr(target), _ptr(grad), _ptr(loss),
+                                          _ptr(bias_grad), _dtype(a), ROUNDINGS[rounding], _ptr(ws), ws.numel(),
+                                          _stream(stream)))
+    return output, grad, loss, bias_grad
 
 
 def tfd_loss_workspace_size(count, dtype) -> int:

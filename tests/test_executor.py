@@ -7,7 +7,7 @@ import itertools
 import pytest
 
 from paper_1603_04467_amd import executor, workloads
-from paper_1603_04467_amd.step import fused_below, op_graph
+from paper_1603_04467_amd.step import fused_below, fused_top, op_graph
 
 
 class _N:
@@ -61,6 +61,8 @@ def test_step_graph_orders_updates_after_reads(name, fuse):
     L = w.layers
 
     def dy_producer(l):   # the op that writes layer l's masked gradient and db
+        if l == L and fused_top(w, fuse):
+            return f"fwd{L}"
         return f"dx{l + 1}" if fused_below(w, l, fuse) else f"relugrad{l}"
 
     for l in range(1, L + 1):
@@ -77,8 +79,10 @@ def test_step_graph_orders_updates_after_reads(name, fuse):
             assert idx[dy_producer(l)] in anc[dx] and idx[dy_producer(l)] in anc[dw]
         if l < L and not fused_below(w, l, fuse):
             assert idx[f"dx{l + 1}"] in anc[idx[f"relugrad{l}"]]
-    # fused: one op per layer above a Relu layer replaces the relugrad op
-    assert ("relugrad1" in names) == (not fused_below(w, 1, fuse))
+    # fused: one op per layer above a Relu layer replaces the relugrad op,
+    # and the output layer's MatMul also runs the squared-error head
+    assert ("relugrad1" in names) == (not fused_below(w, 1, fuse) and not (L == 1 and fused_top(w, fuse)))
+    assert ("loss" in names) == (w.cost != "upstream" and not fused_top(w, fuse))
     # the forward chain precedes the cost and all of the backward pass
     first_bwd = min(i for i, n in enumerate(names) if not n.startswith("fwd") and n != "loss")
     assert idx[f"fwd{L}"] in anc[first_bwd]

@@ -389,3 +389,57 @@ def test_matmul_relu_grad_bias_add_grad(m, n, k, layout, dt, rounding):
                                          rounding=rounding)
     torch.cuda.synchronize()
     assert torch.equal(db, db3)
+
+
+# ------------------------------------- fused output layer + squared error + BiasAddGrad
+
+@pytest.mark.parametrize("m,n,k,layout,dt,rounding,with_target", [
+    (512, 768, 512, "NT", "bf16", "nearest", True),     # whole 256 tiles: the fused epilogue
+    (1024, 512, 768, "NN", "bf16", "nearest", True),
+    (512, 256, 1024, "TN", "bf16", "nearest", True),
+    (512, 768, 512, "NT", "bf16", "truncate", True),
+    (512, 768, 512, "NT", "bf16", "nearest", False),   # no target: MatMul, then the two calls
+    (300, 200, 136, "NT", "bf16", "nearest", True),     # ragged
+    (256, 1024, 1024, "NN", "f32", "nearest", True),
+    (256, 10, 1024, "NN", "f32", "nearest", False),
+    (0, 64, 32, "NT", "f32", "nearest", True),
+])
+def test_matmul_l2_loss_grad(m, n, k, layout, dt, rounding, with_target):
+    rng = np.random.default_rng([m, n, k, len(layout), dt == "bf16", rounding == "truncate", with_target])
+    ta, tb = layout == "TN", layout == "NT"
+    a_h, a = _host(rng, (k, m) if ta else (m, k), dt)
+    b_h, b = _host(rng, (n, k) if tb else (k, n), dt)
+    t_h, t = _host(rng, (m, n), dt) if with_target else (None, None)
+    bias_h = (rng.standard_normal(n) * 0.5).astype(np.float32)
+    bias = torch.from_numpy(bias_h).to(DEV)
+    out, g = _empty((m, n), dt), _empty((m, n), dt)
+    loss = torch.full((1,), float("nan"), dtype=torch.float64, device=DEV)
+    db = torch.full((n,), float("nan"), device=DEV)
+    T.tfd_matmul_l2_loss_grad(a, b, bias, out, t, g, loss, db, transpose_a=ta, transpose_b=tb, rounding=rounding)
+    # the three calls it replaces
+    out2, g2 = _empty((m, n), dt), _empty((m, n), dt)
+    loss2 = torch.full((1,), float("nan"), dtype=torch.float64, device=DEV)
+    db2 = torch.full((n,), float("nan"), device=DEV)
+    T.tfd_matmul(a, b, out2, transpose_a=ta, transpose_b=tb, bias=bias, epilogue="bias", rounding=rounding)
+    T.tfd_l2_loss_grad(out2, t, g2, loss2)
+    T.tfd_bias_add_grad(g2, db2)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2) and torch.equal(g, g2), "output or gradient differs from the three calls"
+    l1, l2 = loss.item(), loss2.item()
+    assert abs(l1 - l2) <= 1e-10 * max(abs(l2), 1e-300), (l1, l2)   # float64 sums in another order
+    gh = to_f64(g2)
+    assert_close(to_f64(db), oracle.bias_add_grad(gh), max(m, 1) * max(amax(gh), 1e-30), TAU["f32"], "fused db")
+    # against the oracle: output within the GEMM tolerance, gradient exact from the stored output
+    store = "bf16t" if rounding == "truncate" else dt
+    want = oracle.matmul(a_h, b_h, ta, tb, out=store, bias=bias_h.astype(np.float64))
+    assert_close(to_f64(out), want, k * amax(a_h) * amax(b_h) + amax(bias_h), TAU[dt], "fused output")
+    g_want, l_want = oracle.l2_loss_grad(to_f64(out), t_h, grad_dtype=dt)
+    assert_bits(gh, g_want, "fused gradient")
+    assert abs(l1 - l_want) <= 1e-6 * max(l_want, 1e-300)
+    # fixed summation order
+    loss3 = torch.empty_like(loss)
+    db3 = torch.empty_like(db)
+    T.tfd_matmul_l2_loss_grad(a, b, bias, torch.empty_like(out), t, torch.empty_like(g), loss3, db3,
+                              transpose_a=ta, transpose_b=tb, rounding=rounding)
+    torch.cuda.synchronize()
+    assert torch.equal(loss, loss3) and torch.equal(db, db3)
