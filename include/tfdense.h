@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TFD_ABI_VERSION 2
+#define TFD_ABI_VERSION 3
 
 #if defined(__GNUC__)
 #define TFD_API __attribute__((visibility("default")))
@@ -187,6 +187,67 @@ TFD_API tfd_status tfd_matmul_relu_grad_bias_add_grad(int transpose_a, int trans
                                               int64_t ldb, const void* features, void* backprops,
                                               float* bias_grad, tfd_dtype type, tfd_rounding rounding,
                                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ReLU masks
+ * ----------
+ * ReluGrad (section 4.1) needs only one fact about each forward output: is
+ * the stored value > 0. A ReLU mask keeps that fact as one bit per element,
+ * so the backward pass can read 1 bit instead of a 16- or 32-bit feature.
+ * Layout of the mask of a rows x cols matrix: rows x ceil(cols / 32) uint32
+ * words, contiguous (row r starts at word r * ceil(cols / 32)); bit j of
+ * word w of row r is 1 iff element (r, 32 w + j) is > 0 (so -0, +0 and NaN
+ * give 0); the bits past the last column of a row are 0. Masks are 4-byte
+ * aligned device buffers owned by the caller. A mask-based call stores
+ * exactly what its features-based counterpart stores, bit for bit.
+ */
+
+/* relu_mask = the mask of features (rows x cols of `type`, contiguous). */
+TFD_API tfd_status tfd_relu_mask(const void* features, uint32_t* relu_mask, int64_t rows, int64_t cols,
+                                 tfd_dtype type, void* stream);
+
+/*
+ * The forward MatMul + Add + ReLU of Figure 1 that also emits the ReLU mask
+ * of its output (for the layer's ReluGrad in the backward pass):
+ *   c = Relu(op(A) op(B) + 1 bias^T), as tfd_matmul with TFD_EPI_BIAS_RELU
+ *       (and TFD_EPI_TRUNCATE_16 when rounding is TFD_ROUND_TRUNCATE), with
+ *       A, B and c all of `type`,
+ *   relu_mask = the mask of the stored c (m rows, ceil(n / 32) words each).
+ * c is bit-identical to tfd_matmul's. bias is fp32[n] and required. The
+ * mask must not overlap A, B, bias or c.
+ */
+TFD_API tfd_status tfd_matmul_relu_mask(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                        const void* a, int64_t lda, const void* b, int64_t ldb,
+                                        const float* bias, void* c, int64_t ldc, uint32_t* relu_mask,
+                                        tfd_dtype type, tfd_rounding rounding, void* stream);
+
+/*
+ * tfd_relu_grad_bias_add_grad with the Relu test read from a ReLU mask of
+ * the rows x cols forward output (instead of the features themselves):
+ *   d = bit(r, c) ? gradients[r, c] : +0, backprops = d (skipped when
+ *   backprops is NULL), bias_grad[c] = sum_r d.
+ * backprops and bias_grad equal tfd_relu_grad_bias_add_grad's bit for bit
+ * when relu_mask is the mask of its features. Workspace as
+ * tfd_reduction_workspace_size. No output may overlap an input.
+ */
+TFD_API tfd_status tfd_relu_mask_grad_bias_add_grad(const void* gradients, const uint32_t* relu_mask,
+                                                    void* backprops, float* bias_grad, int64_t rows,
+                                                    int64_t cols, tfd_dtype type, void* workspace,
+                                                    size_t workspace_bytes, void* stream);
+
+/*
+ * tfd_matmul_relu_grad_bias_add_grad with the Relu test read from a ReLU
+ * mask of the m x n forward output instead of its features. backprops equals
+ * the features-based call's bit for bit (and bias_grad too, on the same
+ * shapes). Workspace as tfd_matmul_relu_grad_workspace_size.
+ */
+TFD_API tfd_status tfd_matmul_relu_mask_grad_bias_add_grad(int transpose_a, int transpose_b, int64_t m,
+                                                           int64_t n, int64_t k, const void* a, int64_t lda,
+                                                           const void* b, int64_t ldb,
+                                                           const uint32_t* relu_mask, void* backprops,
+                                                           float* bias_grad, tfd_dtype type,
+                                                           tfd_rounding rounding, void* workspace,
+                                                           size_t workspace_bytes, void* stream);
 
 /* Workspace bytes that tfd_l2_loss_grad needs for `count` elements. */
 TFD_API size_t tfd_loss_workspace_size(int64_t count, tfd_dtype type);

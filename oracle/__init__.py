@@ -35,6 +35,8 @@ from .dense import (  # noqa: F401
     bias_add,
     relu,
     relu_grad,
+    relu_mask,
+    relu_grad_from_mask,
     bias_add_grad,
     l2_loss_grad,
     softmax,

@@ -146,6 +146,35 @@ def relu_grad(gradients, features):
     return np.where(f > 0.0, g, 0.0)
 
 
+def relu_mask(features):
+    """The test that ReluGrad applies to the stored forward output,
+    ``features > 0``, kept as one bit per element (a storage form of the
+    same predicate; the backward pass then reads bits instead of features).
+
+    Row r of the result holds ``ceil(cols / 32)`` uint32 words; bit j of word
+    w is 1 iff ``features[r, 32 w + j] > 0`` (so -0, +0 and NaN give 0), and
+    the bits past the last column are 0.
+    """
+    f = np.asarray(features, dtype=np.float64)
+    rows, cols = f.shape
+    words = np.zeros((rows, (cols + 31) // 32), dtype=np.uint32)
+    for c in range(cols):
+        words[:, c // 32] |= (f[:, c] > 0.0).astype(np.uint32) << np.uint32(c % 32)
+    return words
+
+
+def relu_grad_from_mask(gradients, mask):
+    """ReluGrad with its test read from a mask made by ``relu_mask``:
+    ``gradients`` where the element's bit is 1, +0 elsewhere."""
+    g = np.asarray(gradients, dtype=np.float64)
+    rows, cols = g.shape
+    m = np.asarray(mask, dtype=np.uint32)
+    keep = np.zeros((rows, cols), dtype=bool)
+    for c in range(cols):
+        keep[:, c] = ((m[:, c // 32] >> np.uint32(c % 32)) & np.uint32(1)) == 1
+    return np.where(keep, g, 0.0)
+
+
 def bias_add_grad(out_backprop, out="f32"):
     """Gradient of the broadcast Add with respect to the bias: the sum of
     the upstream gradient over the broadcast (batch) dimension,

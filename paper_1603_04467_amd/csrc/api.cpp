@@ -280,6 +280,179 @@ tfd_status tfd_matmul_relu_grad_bias_add_grad(int transpose_a, int transpose_b, 
                     "tfd_matmul_relu_grad_bias_add_grad launch");
 }
 
+tfd_status tfd_relu_mask(const void* features, uint32_t* relu_mask, int64_t rows, int64_t cols, tfd_dtype type,
+                         void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_relu_mask";
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (rows == 0 || cols == 0) return TFD_OK;
+  if (!features || !relu_mask) return fail(TFD_EINVAL, "%s: NULL pointer", fn);
+  const size_t fb = (size_t)rows * (size_t)cols * elem_bytes(type), mb = (size_t)rows * ((cols + 31) / 32) * 4;
+  if (overlaps(features, fb, relu_mask, mb)) return fail(TFD_EINVAL, "%s: relu_mask overlaps features", fn);
+  if ((reinterpret_cast<uintptr_t>(relu_mask) & 3) != 0) return fail(TFD_EINVAL, "%s: relu_mask not 4-byte aligned", fn);
+  return hip_status(tfd::launch_relu_mask(features, cols, relu_mask, (cols + 31) / 32, rows, cols, type == TFD_BF16,
+                                          as_stream(stream)),
+                    "tfd_relu_mask launch");
+}
+
+tfd_status tfd_matmul_relu_mask(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k, const void* a,
+                                int64_t lda, const void* b, int64_t ldb, const float* bias, void* c, int64_t ldc,
+                                uint32_t* relu_mask, tfd_dtype type, tfd_rounding rounding, void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_matmul_relu_mask";
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "%s: unknown rounding", fn);
+  if (rounding == TFD_ROUND_TRUNCATE && type != TFD_BF16)
+    return fail(TFD_EINVAL, "%s: truncation needs a 16-bit output", fn);
+  if (transpose_a && transpose_b) return fail(TFD_EUNSUPPORTED, "%s: transpose_a and transpose_b together", fn);
+  if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30)) return fail(TFD_EUNSUPPORTED, "%s: dimension above 2^30", fn);
+  const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
+  const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
+  if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1) || ldc < (n > 0 ? n : 1))
+    return fail(TFD_EINVAL, "%s: leading dimension smaller than the row", fn);
+  if (m == 0 || n == 0) return TFD_OK;
+  if (!c || !bias || !relu_mask) return fail(TFD_EINVAL, "%s: c, bias or relu_mask is NULL", fn);
+  if (k > 0 && (!a || !b)) return fail(TFD_EINVAL, "%s: a or b is NULL", fn);
+  if ((reinterpret_cast<uintptr_t>(relu_mask) & 3) != 0) return fail(TFD_EINVAL, "%s: relu_mask not 4-byte aligned", fn);
+  const int eb = elem_bytes(type);
+  const int64_t ldm = (n + 31) / 32;
+  const size_t c_span = span(m, n, ldc, eb), mb = (size_t)m * (size_t)ldm * 4, nb = (size_t)n * 4;
+  const size_t as = span(a_rows, a_cols, lda, eb), bs = span(b_rows, b_cols, ldb, eb);
+  if (overlaps(c, c_span, a, as) || overlaps(c, c_span, b, bs) || overlaps(c, c_span, bias, nb) ||
+      overlaps(relu_mask, mb, a, as) || overlaps(relu_mask, mb, b, bs) || overlaps(relu_mask, mb, bias, nb) ||
+      overlaps(relu_mask, mb, c, c_span))
+    return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.a = a;
+  d.lda = lda;
+  d.b = b;
+  d.ldb = ldb;
+  d.c = c;
+  d.ldc = ldc;
+  d.in_bf16 = type == TFD_BF16;
+  d.out_bf16 = type == TFD_BF16;
+  d.bias = bias;
+  d.epi = TFD_EPI_BIAS_RELU | (rounding == TFD_ROUND_TRUNCATE ? tfd::kEpiTrunc16 : 0);
+  d.mask_out = relu_mask;
+  d.ldm = ldm;
+  hipStream_t s = as_stream(stream);
+  if (tfd::gemm_bf16_256_ok(d) && tfd::gemm_tile_override() == 0)
+    return hip_status(tfd::launch_gemm_bf16_256(d, s), "tfd_matmul_relu_mask launch");
+  // other shapes: the MatMul, then the mask of its stored output
+  d.mask_out = nullptr;
+  hipError_t e = tfd::launch_gemm(d, s);
+  if (e == hipSuccess) e = tfd::launch_relu_mask(c, ldc, relu_mask, ldm, m, n, type == TFD_BF16, s);
+  return hip_status(e, "tfd_matmul_relu_mask launch");
+}
+
+tfd_status tfd_relu_mask_grad_bias_add_grad(const void* gradients, const uint32_t* relu_mask, void* backprops,
+                                            float* bias_grad, int64_t rows, int64_t cols, tfd_dtype type,
+                                            void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_relu_mask_grad_bias_add_grad";
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (cols == 0) return TFD_OK;
+  if (!bias_grad) return fail(TFD_EINVAL, "%s: bias_grad is NULL", fn);
+  if (rows > 0 && (!gradients || !relu_mask)) return fail(TFD_EINVAL, "%s: gradients or relu_mask is NULL", fn);
+  if (relu_mask && (reinterpret_cast<uintptr_t>(relu_mask) & 3) != 0)
+    return fail(TFD_EINVAL, "%s: relu_mask not 4-byte aligned", fn);
+  const size_t need = tfd::reduction_ws_bytes(rows, cols, type == TFD_BF16);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need, workspace_bytes);
+  const int64_t ldm = (cols + 31) / 32;
+  const size_t bytes = (size_t)(rows * cols) * elem_bytes(type), mb = (size_t)rows * ldm * 4;
+  if (overlaps(backprops, bytes, gradients, bytes) || overlaps(backprops, bytes, relu_mask, mb) ||
+      overlaps(workspace, need, gradients, bytes) || overlaps(workspace, need, backprops, bytes) ||
+      overlaps(workspace, need, relu_mask, mb) || overlaps(bias_grad, (size_t)cols * 4, backprops, bytes) ||
+      overlaps(bias_grad, (size_t)cols * 4, workspace, need) || overlaps(bias_grad, (size_t)cols * 4, relu_mask, mb))
+    return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+  return hip_status(tfd::launch_relu_mask_grad_bias_add_grad(gradients, relu_mask, ldm, backprops, bias_grad, rows, cols,
+                                                             type == TFD_BF16, workspace, as_stream(stream)),
+                    "tfd_relu_mask_grad_bias_add_grad launch");
+}
+
+tfd_status tfd_matmul_relu_mask_grad_bias_add_grad(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                                   const void* a, int64_t lda, const void* b, int64_t ldb,
+                                                   const uint32_t* relu_mask, void* backprops, float* bias_grad,
+                                                   tfd_dtype type, tfd_rounding rounding, void* workspace,
+                                                   size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_matmul_relu_mask_grad_bias_add_grad";
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (!valid_rounding(rounding)) return fail(TFD_EINVAL, "%s: unknown rounding", fn);
+  if (rounding == TFD_ROUND_TRUNCATE && type != TFD_BF16)
+    return fail(TFD_EINVAL, "%s: truncation needs a 16-bit output", fn);
+  if (transpose_a && transpose_b) return fail(TFD_EUNSUPPORTED, "%s: transpose_a and transpose_b together", fn);
+  if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30)) return fail(TFD_EUNSUPPORTED, "%s: dimension above 2^30", fn);
+  const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
+  const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
+  if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1))
+    return fail(TFD_EINVAL, "%s: leading dimension smaller than the row", fn);
+  if (n == 0) return TFD_OK;
+  if (!bias_grad) return fail(TFD_EINVAL, "%s: bias_grad is NULL", fn);
+  const size_t need = tfd_matmul_relu_grad_workspace_size(m, n, type);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "%s: workspace of %zu bytes needed, %zu given", fn, need, workspace_bytes);
+  if (m > 0 && (!relu_mask || !backprops || (k > 0 && (!a || !b)))) return fail(TFD_EINVAL, "%s: NULL pointer", fn);
+  if (relu_mask && (reinterpret_cast<uintptr_t>(relu_mask) & 3) != 0)
+    return fail(TFD_EINVAL, "%s: relu_mask not 4-byte aligned", fn);
+  const int eb = elem_bytes(type);
+  const int64_t ldm = (n + 31) / 32;
+  const size_t c_span = (size_t)m * (size_t)n * eb, mb = (size_t)m * ldm * 4, nb = (size_t)n * 4;
+  if (overlaps(backprops, c_span, a, span(a_rows, a_cols, lda, eb)) ||
+      overlaps(backprops, c_span, b, span(b_rows, b_cols, ldb, eb)) || overlaps(backprops, c_span, relu_mask, mb) ||
+      overlaps(backprops, c_span, bias_grad, nb) || overlaps(backprops, c_span, workspace, need) ||
+      overlaps(bias_grad, nb, workspace, need) || overlaps(bias_grad, nb, relu_mask, mb) ||
+      overlaps(workspace, need, relu_mask, mb))
+    return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+  hipStream_t st = as_stream(stream);
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  d.a = a;
+  d.lda = lda;
+  d.b = b;
+  d.ldb = ldb;
+  d.c = backprops;
+  d.ldc = n;
+  d.in_bf16 = type == TFD_BF16;
+  d.out_bf16 = type == TFD_BF16;
+  d.bias = nullptr;
+  d.epi = rounding == TFD_ROUND_TRUNCATE ? tfd::kEpiTrunc16 : 0;
+  d.mask_in = relu_mask;
+  d.ldm = ldm;
+  d.col_partial = static_cast<float*>(workspace);
+  if (m > 0 && tfd::gemm_bf16_256_ok(d) && tfd::gemm_tile_override() == 0) {
+    hipError_t e = tfd::launch_gemm_bf16_256(d, st);
+    if (e != hipSuccess) return hip_status(e, "tfd_matmul_relu_mask_grad_bias_add_grad launch");
+    return hip_status(tfd::launch_colsum_final(static_cast<const float*>(workspace), bias_grad, m / 256, n, st),
+                      "tfd_matmul_relu_mask_grad_bias_add_grad launch");
+  }
+  // other shapes: the MatMul writes G into backprops, then ReluGrad (from the
+  // mask) and BiasAddGrad run in place over it
+  d.mask_in = nullptr;
+  d.col_partial = nullptr;
+  if (m > 0) {
+    hipError_t e = tfd::launch_gemm(d, st);
+    if (e != hipSuccess) return hip_status(e, "tfd_matmul_relu_mask_grad_bias_add_grad launch");
+  }
+  return hip_status(tfd::launch_relu_mask_grad_bias_add_grad(backprops, relu_mask, ldm, backprops, bias_grad, m, n,
+                                                             type == TFD_BF16, workspace, st),
+                    "tfd_matmul_relu_mask_grad_bias_add_grad launch");
+}
+
 size_t tfd_matmul_l2_loss_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type) {
   if (m < 0 || n < 0 || !valid_dtype(type)) return 0;
   const bool h = type == TFD_BF16;

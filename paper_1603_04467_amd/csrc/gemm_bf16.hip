@@ -57,10 +57,15 @@ struct Params {
   const uint16_t* target;    // squared-error epilogue: target and gradient (ld = n)
   uint16_t* grad;
   double* loss_partial;      // [tiles] float64 sums of squared differences
+  // ReLU masks, one bit per element: row r of a mask is ldm uint32 words,
+  // bit j of word w holds element (r, 32 w + j).
+  const uint32_t* mask_in;   // ReluGrad epilogue from a mask instead of features
+  uint32_t* mask_out;        // forward epilogue: bits of the stored output's > 0
+  int64_t ldm;
 };
 
 // Epilogues of the whole-tile kernel beyond bias/ReLU (16-bit outputs only).
-constexpr int kEpPlain = 0, kEpReluGrad = 1, kEpLoss = 2;
+constexpr int kEpPlain = 0, kEpReluGrad = 1, kEpLoss = 2, kEpReluGradBits = 3, kEpMaskOut = 4;
 
 __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
 __device__ __forceinline__ int swz_mn(int krow) { return (krow & 3) << 2; }
@@ -151,6 +156,9 @@ __device__ __forceinline__ void interleave_mfma_reads() {
 //  kEpReluGrad: the stored value is the rounded product where the matching
 //    feature is > 0 and +0 elsewhere; the tile's column sums of the stored
 //    values go to col_partial (the first pass of BiasAddGrad);
+//  kEpReluGradBits: the same with the feature test read from a ReLU mask;
+//  kEpMaskOut: the output is stored and so is its ReLU mask (bit set where
+//    the stored value is > 0);
 //  kEpLoss: the output is stored, and also grad = output - target (fp32
 //    difference, rounded to nearest even), the tile's float64 sum of squared
 //    differences (loss_partial) and its column sums of grad (col_partial).
@@ -236,6 +244,17 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     // row-chunk reads are free of bank conflicts), then leaves in coalesced
     // 16-byte row chunks. The k loop's last barrier has passed, but waves may
     // still be reading their last fragments: wait for all of them first.
+    constexpr int kRowStep = kThreads / 32;
+    constexpr int kRowIters = kBM / kRowStep;
+    const int cc = tid & 31;  // 16-byte chunk of a row: columns 8cc .. 8cc+7
+    // ReLU mask words of this thread's rows, fetched before the staging so
+    // their latency overlaps it; the byte (cc & 3) of a word covers the chunk.
+    uint32_t mw[EP == kEpReluGradBits ? kRowIters : 1];
+    if constexpr (EP == kEpReluGradBits) {
+#pragma unroll
+      for (int it = 0; it < kRowIters; ++it)
+        mw[it] = p.mask_in[(int64_t)(m0 + (tid >> 5) + it * kRowStep) * p.ldm + (n0 >> 5) + (cc >> 2)];
+    }
     __syncthreads();
     char* tile = smem;  // 256 rows x 512 bytes
 #pragma unroll
@@ -254,13 +273,13 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
       }
     }
     __syncthreads();
-    constexpr int kRowStep = kThreads / 32;
-    const int cc = tid & 31;  // 16-byte chunk of the row: columns 8cc .. 8cc+7
     float cs[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) cs[e] = 0.0f;
     double sq = 0.0;
-    for (int row = tid >> 5; row < kBM; row += kRowStep) {
+#pragma unroll
+    for (int it = 0; it < kRowIters; ++it) {
+      const int row = (tid >> 5) + it * kRowStep;
       u32x4 v = *reinterpret_cast<const u32x4*>(tile + epi_off(row, 8 * cc));
       const int64_t at = (int64_t)(m0 + row) * p.n + n0 + 8 * cc;  // contiguous side buffers
       if constexpr (EP == kEpLoss) {
@@ -292,9 +311,33 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
           cs[2 * e + 1] += bf16_bits_to_f32(hi >> 16);
         }
       }
+      if constexpr (EP == kEpReluGradBits) {
+        const uint32_t bits = mw[it] >> (8 * (cc & 3));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t lo = (bits >> (2 * e)) & 1u ? (v[e] & 0xFFFFu) : 0u;
+          const uint32_t hi = (bits >> (2 * e + 1)) & 1u ? (v[e] & 0xFFFF0000u) : 0u;
+          v[e] = lo | hi;
+          cs[2 * e] += bf16_bits_to_f32(lo);
+          cs[2 * e + 1] += bf16_bits_to_f32(hi >> 16);
+        }
+      }
+      if constexpr (EP == kEpMaskOut) {
+        // 8 bits of this chunk, gathered into one word per 4 neighbouring lanes
+        uint32_t bits = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          bits |= (bf16_bits_to_f32(v[e] & 0xFFFFu) > 0.0f ? 1u : 0u) << (2 * e);
+          bits |= (bf16_bits_to_f32(v[e] >> 16) > 0.0f ? 1u : 0u) << (2 * e + 1);
+        }
+        uint32_t word = bits << (8 * (cc & 3));
+        word |= __shfl_xor(word, 1);
+        word |= __shfl_xor(word, 2);
+        if ((cc & 3) == 0) p.mask_out[(int64_t)(m0 + row) * p.ldm + (n0 >> 5) + (cc >> 2)] = word;
+      }
       *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc) = v;
     }
-    if constexpr (EP != kEpPlain) {
+    if constexpr (EP == kEpReluGrad || EP == kEpReluGradBits || EP == kEpLoss) {
       // column sums: each thread's rows, then the kRowStep threads of a
       // chunk in row-group order (a fixed order)
       __syncthreads();
@@ -369,8 +412,15 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.target = static_cast<const uint16_t*>(d.target);
   p.grad = static_cast<uint16_t*>(d.grad);
   p.loss_partial = d.loss_partial;
+  p.mask_in = d.mask_in;
+  p.mask_out = d.mask_out;
+  p.ldm = d.ldm;
   dim3 grid(p.tiles_m * p.tiles_n), block(64 * WM * WN);
-  if (d.features)
+  if (d.mask_in)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpReluGradBits>), grid, block, 0, s, p);
+  else if (d.mask_out)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpMaskOut>), grid, block, 0, s, p);
+  else if (d.features)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpReluGrad>), grid, block, 0, s, p);
   else if (d.target)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpLoss>), grid, block, 0, s, p);
@@ -407,8 +457,10 @@ bool gemm_bf16_256_ok(const GemmDesc& d) {
   const bool c_ok = !d.out_bf16 || (al(d.c) && d.ldc % 8 == 0);
   const bool f_ok = !d.features || (al(d.features) && d.ldf % 8 == 0);
   const bool l_ok = !d.target || (al(d.target) && al(d.grad) && d.n % 8 == 0);
+  // mask epilogues write or read whole words of 16-bit tiles
+  const bool m_ok = (!d.mask_in && !d.mask_out) || (d.out_bf16 && d.ldm >= d.n / 32);
   return d.in_bf16 && d.m % kBM == 0 && d.n % kBN == 0 && d.k % kBK == 0 && d.k > 0 &&
-         gemm_vector_ok(d, 2) && !(d.ta && d.tb) && c_ok && f_ok && l_ok;
+         gemm_vector_ok(d, 2) && !(d.ta && d.tb) && c_ok && f_ok && l_ok && m_ok;
 }
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {

@@ -34,6 +34,12 @@ struct GemmDesc {
   const void* target = nullptr;
   void* grad = nullptr;
   double* loss_partial = nullptr;
+  // ReLU masks (16-bit whole-tile kernel only), one bit per element, row r
+  // at word r * ldm: mask_in replaces features in the ReluGrad epilogue;
+  // mask_out receives the bits of the stored output's > 0 test.
+  const uint32_t* mask_in = nullptr;
+  uint32_t* mask_out = nullptr;
+  int64_t ldm = 0;
 };
 
 constexpr int kEpiOpMask = 3;
@@ -62,6 +68,13 @@ size_t reduction_ws_bytes(int64_t rows, int64_t cols, bool bf16);
 hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* out, float* db,
                                           int64_t rows, int64_t cols, bool bf16, void* ws,
                                           hipStream_t s);
+// The same with the Relu test read from a bit mask (rows x ldm words).
+hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,
+                                               float* db, int64_t rows, int64_t cols, bool bf16, void* ws,
+                                               hipStream_t s);
+// mask[r * ldm + w] bit j = x[r * ldx + 32 w + j] > 0 (bits past cols are 0).
+hipError_t launch_relu_mask(const void* x, int64_t ldx, uint32_t* mask, int64_t ldm, int64_t rows, int64_t cols,
+                            bool bf16, hipStream_t s);
 
 size_t loss_ws_bytes(int64_t count, bool bf16);
 hipError_t launch_l2_loss_grad(const void* out, const void* target, void* grad, double* loss,

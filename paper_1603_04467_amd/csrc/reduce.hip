@@ -1,7 +1,9 @@
 // BiasAddGrad (the bias gradient of the broadcast Add, section 4.1 of the
 // paper), optionally fused with ReluGrad: one pass over the upstream
 // gradient G (and the stored Relu output H) that writes the masked gradient
-// dY and reduces it over the batch rows.
+// dY and reduces it over the batch rows. The Relu test comes either from H
+// (H > 0) or from a ReLU mask that holds the same test as one bit per
+// element (written by the forward MatMul, or by relu_mask_kernel below).
 //
 // Pass 1 (grid: column groups x row chunks): each thread owns one 16-byte
 // column chunk (4 fp32 / 8 bf16 columns) and walks the rows of its chunk with
@@ -82,10 +84,18 @@ template <> struct Chunk16<bf16> {
 __device__ __forceinline__ float masked(float g, float f) {
   return __builtin_bit_cast(float, f > 0.0f ? __builtin_bit_cast(uint32_t, g) : 0u);
 }
+__device__ __forceinline__ float kept(float g, uint32_t bit) {
+  return __builtin_bit_cast(float, bit ? __builtin_bit_cast(uint32_t, g) : 0u);
+}
 
-template <typename T, bool MASK, bool WRITE, bool VEC>
+// Where the Relu test comes from: none (BiasAddGrad alone), the stored
+// features (f > 0), or a bit mask (bit (r, c) of mb, row r at word r * ldm).
+constexpr int kNoMask = 0, kFeatures = 1, kBits = 2;
+
+template <typename T, int MASK, bool WRITE, bool VEC>
 __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __restrict__ g,
                                                                   const T* __restrict__ f,
+                                                                  const uint32_t* __restrict__ mb, int64_t ldm,
                                                                   T* __restrict__ out,
                                                                   float* __restrict__ partial, int64_t rows,
                                                                   int64_t cols, int64_t rows_per_chunk) {
@@ -112,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
         float x[U][V];
 #pragma unroll
         for (int u = 0; u < U; ++u) Chunk16<T>::load(g + (r + u * kRowPhases) * cols + c0, x[u]);
-        if (MASK) {
+        if (MASK == kFeatures) {
           float m[U][V];
 #pragma unroll
           for (int u = 0; u < U; ++u) Chunk16<T>::load(f + (r + u * kRowPhases) * cols + c0, m[u]);
@@ -120,6 +130,16 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
           for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int e = 0; e < V; ++e) x[u][e] = masked(x[u][e], m[u][e]);
+        }
+        if (MASK == kBits) {
+          // the chunk's V bits lie in one word (c0 is a multiple of V)
+          uint32_t w[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) w[u] = mb[(r + u * kRowPhases) * ldm + (c0 >> 5)] >> (c0 & 31);
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < V; ++e) x[u][e] = kept(x[u][e], (w[u] >> e) & 1u);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -134,11 +154,16 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
       float x[V];
       if (full) {
         Chunk16<T>::load(g + base, x);
-        if (MASK) {
+        if (MASK == kFeatures) {
           float m[V];
           Chunk16<T>::load(f + base, m);
 #pragma unroll
           for (int e = 0; e < V; ++e) x[e] = masked(x[e], m[e]);
+        }
+        if (MASK == kBits) {
+          const uint32_t w = mb[r * ldm + (c0 >> 5)] >> (c0 & 31);
+#pragma unroll
+          for (int e = 0; e < V; ++e) x[e] = kept(x[e], (w >> e) & 1u);
         }
         if (WRITE) Chunk16<T>::store(out + base, x);
 #pragma unroll
@@ -148,7 +173,8 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
         for (int e = 0; e < V; ++e) {
           if (c0 + e < cols) {
             float v = load_f32(g + base + e);
-            if (MASK) v = masked(v, load_f32(f + base + e));
+            if (MASK == kFeatures) v = masked(v, load_f32(f + base + e));
+            if (MASK == kBits) v = kept(v, (mb[r * ldm + ((c0 + e) >> 5)] >> ((c0 + e) & 31)) & 1u);
             if (WRITE) store_from_f32(out + base + e, v);
             acc[e] += v;
           }
@@ -167,6 +193,38 @@ __global__ __launch_bounds__(kThreads) void colsum_partial_kernel(const T* __res
       for (int ph = 1; ph < kRowPhases; ++ph) s += sh[ph][i];
       partial[chunk * cols + c] = s;
     }
+  }
+}
+
+// ReLU mask: one thread per 32-column word of a row; bit j is set when
+// element 32 w + j is > 0 (the test ReluGrad applies to the stored forward
+// output). VEC: the row's 32 values are read as 16-byte chunks (cols a
+// multiple of 32, aligned rows); otherwise per element, with the bits past
+// the last column left 0.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kThreads) void relu_mask_kernel(const T* __restrict__ x, int64_t ldx,
+                                                             uint32_t* __restrict__ mask, int64_t ldm,
+                                                             int64_t rows, int64_t cols) {
+  const int64_t words = (cols + 31) / 32;
+  const int64_t total = rows * words;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
+    const int64_t r = i / words, w = i - r * words;
+    const T* row = x + r * ldx + w * 32;
+    uint32_t bits = 0;
+    if (VEC) {
+      constexpr int V = Chunk16<T>::V;
+#pragma unroll
+      for (int c = 0; c < 32 / V; ++c) {
+        float v[V];
+        Chunk16<T>::load(row + c * V, v);
+#pragma unroll
+        for (int e = 0; e < V; ++e) bits |= (v[e] > 0.0f ? 1u : 0u) << (c * V + e);
+      }
+    } else {
+      const int n = (int)min<int64_t>(32, cols - w * 32);
+      for (int e = 0; e < n; ++e) bits |= (load_f32(row + e) > 0.0f ? 1u : 0u) << e;
+    }
+    mask[r * ldm + w] = bits;
   }
 }
 
@@ -192,27 +250,40 @@ __global__ __launch_bounds__(kThreads) void colsum_final_kernel(const float* par
 }
 
 template <typename T>
-hipError_t launch_t(const T* g, const T* f, T* out, float* db, int64_t rows, int64_t cols, float* ws,
-                    hipStream_t s) {
+hipError_t launch_t(const T* g, const T* f, const uint32_t* mb, int64_t ldm, T* out, float* db, int64_t rows,
+                    int64_t cols, float* ws, hipStream_t s) {
   constexpr int V = Chunk16<T>::V;
   const ReducePlan p = plan(rows, cols, V);
   auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
   const bool vec = (cols % V == 0) && al(g) && (!f || al(f)) && (!out || al(out));
   dim3 grid((unsigned)p.col_groups, (unsigned)p.row_chunks);
-#define TFD_LAUNCH(M, W, VE)                                                                      \
-  hipLaunchKernelGGL((colsum_partial_kernel<T, M, W, VE>), grid, kThreads, 0, s, g, f, out, ws, rows, \
+#define TFD_LAUNCH(M, W, VE)                                                                             \
+  hipLaunchKernelGGL((colsum_partial_kernel<T, M, W, VE>), grid, kThreads, 0, s, g, f, mb, ldm, out, ws, rows, \
                      cols, p.rows_per_chunk)
-  const bool mask = f != nullptr, write = out != nullptr;
+  const int mode = mb ? kBits : (f ? kFeatures : kNoMask);
+  const bool write = out != nullptr;
   if (vec) {
-    if (mask && write) TFD_LAUNCH(true, true, true);
-    else if (mask) TFD_LAUNCH(true, false, true);
-    else if (write) TFD_LAUNCH(false, true, true);
-    else TFD_LAUNCH(false, false, true);
+    if (mode == kBits) {
+      if (write) TFD_LAUNCH(kBits, true, true);
+      else TFD_LAUNCH(kBits, false, true);
+    } else if (mode == kFeatures) {
+      if (write) TFD_LAUNCH(kFeatures, true, true);
+      else TFD_LAUNCH(kFeatures, false, true);
+    } else {
+      if (write) TFD_LAUNCH(kNoMask, true, true);
+      else TFD_LAUNCH(kNoMask, false, true);
+    }
   } else {
-    if (mask && write) TFD_LAUNCH(true, true, false);
-    else if (mask) TFD_LAUNCH(true, false, false);
-    else if (write) TFD_LAUNCH(false, true, false);
-    else TFD_LAUNCH(false, false, false);
+    if (mode == kBits) {
+      if (write) TFD_LAUNCH(kBits, true, false);
+      else TFD_LAUNCH(kBits, false, false);
+    } else if (mode == kFeatures) {
+      if (write) TFD_LAUNCH(kFeatures, true, false);
+      else TFD_LAUNCH(kFeatures, false, false);
+    } else {
+      if (write) TFD_LAUNCH(kNoMask, true, false);
+      else TFD_LAUNCH(kNoMask, false, false);
+    }
   }
 #undef TFD_LAUNCH
   hipError_t e = hipGetLastError();
@@ -239,8 +310,42 @@ hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* ou
                                           int64_t rows, int64_t cols, bool bf16_t, void* ws,
                                           hipStream_t s) {
   if (bf16_t)
-    return launch_t<bf16>((const bf16*)g, (const bf16*)f, (bf16*)out, db, rows, cols, (float*)ws, s);
-  return launch_t<float>((const float*)g, (const float*)f, (float*)out, db, rows, cols, (float*)ws, s);
+    return launch_t<bf16>((const bf16*)g, (const bf16*)f, nullptr, 0, (bf16*)out, db, rows, cols, (float*)ws, s);
+  return launch_t<float>((const float*)g, (const float*)f, nullptr, 0, (float*)out, db, rows, cols, (float*)ws, s);
+}
+
+hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,
+                                               float* db, int64_t rows, int64_t cols, bool bf16_t, void* ws,
+                                               hipStream_t s) {
+  if (bf16_t)
+    return launch_t<bf16>((const bf16*)g, nullptr, mask, ldm, (bf16*)out, db, rows, cols, (float*)ws, s);
+  return launch_t<float>((const float*)g, nullptr, mask, ldm, (float*)out, db, rows, cols, (float*)ws, s);
+}
+
+hipError_t launch_relu_mask(const void* x, int64_t ldx, uint32_t* mask, int64_t ldm, int64_t rows, int64_t cols,
+                            bool bf16_t, hipStream_t s) {
+  const int64_t total = rows * ((cols + 31) / 32);
+  if (total == 0) return hipSuccess;
+  int64_t blocks = (total + kThreads - 1) / kThreads;
+  if (blocks > 65536) blocks = 65536;  // grid-stride beyond
+  const int eb = bf16_t ? 2 : 4;
+  const bool vec = cols % 32 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (ldx * eb) % 16 == 0;
+  if (bf16_t) {
+    if (vec)
+      hipLaunchKernelGGL((relu_mask_kernel<bf16, true>), (unsigned)blocks, kThreads, 0, s, (const bf16*)x, ldx, mask,
+                         ldm, rows, cols);
+    else
+      hipLaunchKernelGGL((relu_mask_kernel<bf16, false>), (unsigned)blocks, kThreads, 0, s, (const bf16*)x, ldx, mask,
+                         ldm, rows, cols);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((relu_mask_kernel<float, true>), (unsigned)blocks, kThreads, 0, s, (const float*)x, ldx,
+                         mask, ldm, rows, cols);
+    else
+      hipLaunchKernelGGL((relu_mask_kernel<float, false>), (unsigned)blocks, kThreads, 0, s, (const float*)x, ldx,
+                         mask, ldm, rows, cols);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace tfd

@@ -48,15 +48,28 @@ def fused_top(w: Workload, fuse: bool) -> bool:
     return fuse and w.cost in ("sq_err", "half_sq") and not w.relus[-1]
 
 
-def op_graph(w: Workload, fuse: bool = True):
+def default_masks(w: Workload) -> bool:
+    """Whether the step keeps ReLU masks (one bit per element of H > 0) for
+    its ReluGrads by default: with 16-bit activations, where the forward
+    MatMul writes the mask in its epilogue and the backward pass then reads
+    1 bit instead of 16 per element."""
+    return w.act == "bf16"
+
+
+def op_graph(w: Workload, fuse: bool = True, masks: bool = False):
     """(name, reads, writes) of every op of one step of ``w``, in program
     order. Keys name buffers: h<l> activations (h0 = x), g the cost gradient,
     dy<l>/dx<l>/dw<l>/db<l> the gradients of layer l, W<l>/b<l> its Variables
-    (all copies of the weights), ws the shared reduction workspace. With
-    ``fuse``, the input-gradient MatMul of a layer above a Relu layer also
-    produces that layer's dY and db (no separate relugrad op, no stored dX)."""
+    (all copies of the weights), m<l> the ReLU mask of layer l's output, ws
+    the shared reduction workspace. With ``fuse``, the input-gradient MatMul
+    of a layer above a Relu layer also produces that layer's dY and db (no
+    separate relugrad op, no stored dX). With ``masks``, a Relu layer's
+    forward MatMul also writes its mask and its ReluGrad reads the mask
+    instead of the layer's output."""
     L = w.layers
-    ops = [(f"fwd{l + 1}", (f"h{l}", f"W{l}", f"b{l}"), (f"h{l + 1}",)) for l in range(L)]
+    mk = lambda l: masks and w.relus[l]  # noqa: E731
+    ops = [(f"fwd{l + 1}", (f"h{l}", f"W{l}", f"b{l}"), (f"h{l + 1}",) + ((f"m{l}",) if mk(l) else ()))
+           for l in range(L)]
     if fused_top(w, fuse):
         ops[-1] = (f"fwd{L}", (f"h{L - 1}", f"W{L - 1}", f"b{L - 1}", "target"),
                    (f"h{L}", "g", "loss", f"db{L - 1}", "ws"))
@@ -67,9 +80,10 @@ def op_graph(w: Workload, fuse: bool = True):
         dykey = f"dy{l}" if w.relus[l] else gkey
         if not fused_below(w, l + 1, fuse) and not (l == L - 1 and fused_top(w, fuse)):
             rg_writes = (f"dy{l}", f"db{l}", "ws") if w.relus[l] else (f"db{l}", "ws")
-            ops.append((f"relugrad{l + 1}", (gkey, f"h{l + 1}"), rg_writes))
+            ops.append((f"relugrad{l + 1}", (gkey, f"m{l}" if mk(l) else f"h{l + 1}"), rg_writes))
         if fused_below(w, l, fuse):
-            ops.append((f"dx{l + 1}", (dykey, f"W{l}", f"h{l}"), (f"dy{l - 1}", f"db{l - 1}", "ws")))
+            ops.append((f"dx{l + 1}", (dykey, f"W{l}", f"m{l - 1}" if mk(l - 1) else f"h{l}"),
+                        (f"dy{l - 1}", f"db{l - 1}", "ws")))
         else:
             ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}",)))
         ops.append((f"dw{l + 1}", (f"h{l}", dykey), (f"dw{l}",)))
@@ -82,9 +96,10 @@ def op_graph(w: Workload, fuse: bool = True):
 class DenseStep:
     """Device state and launch sequence of one step of workload ``w``."""
 
-    def __init__(self, w: Workload, inputs: dict, device="cuda", fuse: bool = True):
+    def __init__(self, w: Workload, inputs: dict, device="cuda", fuse: bool = True, masks: Optional[bool] = None):
         self.w = w
         self.fuse = fuse
+        self.use_masks = default_masks(w) if masks is None else bool(masks)
         self.device = torch.device(device)
         self.act = torch.bfloat16 if w.act == "bf16" else torch.float32
         dev = self.device
@@ -113,6 +128,9 @@ class DenseStep:
                    for l in range(L)]
         self.dx = [torch.empty(N, w.dims[l], dtype=self.act, device=dev) for l in range(L)]
         self.dw = [torch.empty(w.dims[l], w.dims[l + 1], dtype=torch.float32, device=dev) for l in range(L)]
+        # ReLU masks of the Relu layers' outputs (uint32 words in int32 tensors)
+        self.masks = [T.new_relu_mask(N, w.dims[l + 1], dev) if self.use_masks and w.relus[l] else None
+                      for l in range(L)]
         self.db = [torch.empty(w.dims[l + 1], dtype=torch.float32, device=dev) for l in range(L)]
         self.loss = torch.zeros(1, dtype=torch.float64, device=dev)
 
@@ -159,7 +177,12 @@ class DenseStep:
             epi = "bias_relu" if w.relus[l] else "bias"
 
             def launch(st):
-                if self.weights_t is not None:
+                if self.masks[l] is not None:
+                    wt = self.weights_t is not None
+                    T.tfd_matmul_relu_mask(self.h[l], self.weights_t[l] if wt else self.weights[l], self.biases[l],
+                                           self.h[l + 1], self.masks[l], transpose_b=wt, rounding=w.rounding,
+                                           stream=st)
+                elif self.weights_t is not None:
                     T.tfd_matmul(self.h[l], self.weights_t[l], self.h[l + 1], transpose_b=True, bias=self.biases[l],
                                  epilogue=epi, rounding=w.rounding, stream=st)
                 else:
@@ -190,13 +213,20 @@ class DenseStep:
             dyl = self.dy[l] if w.relus[l] else grad
 
             def relugrad(st):
-                if w.relus[l]:
+                if self.masks[l] is not None:
+                    T.tfd_relu_mask_grad_bias_add_grad(grad, self.masks[l], self.dy[l], self.db[l], workspace=ws,
+                                                       stream=st)
+                elif w.relus[l]:
                     T.tfd_relu_grad_bias_add_grad(grad, self.h[l + 1], self.dy[l], self.db[l], workspace=ws, stream=st)
                 else:
                     T.tfd_bias_add_grad(grad, self.db[l], workspace=ws, stream=st)
 
             def dx(st):
-                if fused_below(w, l, self.fuse):
+                if fused_below(w, l, self.fuse) and self.masks[l - 1] is not None:
+                    T.tfd_matmul_relu_mask_grad_bias_add_grad(dyl, self.weights[l], self.masks[l - 1], self.dy[l - 1],
+                                                              self.db[l - 1], transpose_b=True, rounding=w.rounding,
+                                                              workspace=ws, stream=st)
+                elif fused_below(w, l, self.fuse):
                     T.tfd_matmul_relu_grad_bias_add_grad(dyl, self.weights[l], self.h[l], self.dy[l - 1], self.db[l - 1],
                                                          transpose_b=True, rounding=w.rounding, workspace=ws,
                                                          stream=st)
@@ -220,7 +250,8 @@ class DenseStep:
         for l in reversed(range(L)):
             backward(l, grad)
             grad = self.dx[l]
-        return [Node(name, launches[name], reads, writes) for name, reads, writes in op_graph(w, self.fuse)]
+        return [Node(name, launches[name], reads, writes)
+                for name, reads, writes in op_graph(w, self.fuse, self.use_masks)]
 
     def run(self, mark=None, stream=None):
         """Enqueue one step in program order on one stream (the current one

@@ -36,6 +36,8 @@ EXPORTS = (
     "tfd_matmul_l2_loss_grad_workspace_size", "tfd_matmul_l2_loss_grad", "tfd_loss_workspace_size", "tfd_l2_loss_grad",
     "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent",
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
+    "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
+    "tfd_matmul_relu_mask_grad_bias_add_grad",
 )
 
 
@@ -83,6 +85,11 @@ def load() -> ctypes.CDLL:
         "tfd_apply_gradient_descent_matrix": ([vp, ctypes.c_float, vp, i64, i64, vp, vp, i32, vp], i32),
         "tfd_convert_f32_to_bf16": ([vp, vp, i64, i32, vp], i32),
         "tfd_convert_bf16_to_f32": ([vp, vp, i64, vp], i32),
+        "tfd_relu_mask": ([vp, vp, i64, i64, i32, vp], i32),
+        "tfd_matmul_relu_mask": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, vp, i32, i32, vp], i32),
+        "tfd_relu_mask_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
+        "tfd_matmul_relu_mask_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32,
+                                                     vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -207,6 +214,91 @@ def tfd_matmul_relu_grad_bias_add_grad(a, b, features, backprops, bias_grad, tra
                                                      _ptr(b), ldb, _ptr(features), _ptr(backprops), _ptr(bias_grad),
                                                      _dtype(a), ROUNDINGS[rounding], _ptr(ws), ws.numel(),
                                                      _stream(stream)))
+    return backprops, bias_grad
+
+
+def relu_mask_words(cols: int) -> int:
+    """uint32 words per row of a ReLU mask of a matrix with ``cols`` columns."""
+    return (cols + 31) // 32
+
+
+def new_relu_mask(rows: int, cols: int, device) -> torch.Tensor:
+    """An uninitialised ReLU mask buffer (int32 words holding the uint32 bits)."""
+    return torch.empty(rows, relu_mask_words(cols), dtype=torch.int32, device=device)
+
+
+def _mask(mask: torch.Tensor, rows: int, cols: int):
+    if mask.dtype != torch.int32 or tuple(mask.shape) != (rows, relu_mask_words(cols)) or not mask.is_contiguous():
+        raise ValueError(f"relu_mask must be a contiguous int32 [{rows}, {relu_mask_words(cols)}] tensor")
+
+
+def tfd_relu_mask(features, relu_mask, stream=None):
+    """relu_mask = one bit per element of features > 0 (see include/tfdense.h)."""
+    rows, cols = features.shape
+    _flat(features, "features")
+    _mask(relu_mask, rows, cols)
+    _check(load().tfd_relu_mask(_ptr(features), _ptr(relu_mask), rows, cols, _dtype(features), _stream(stream)))
+    return relu_mask
+
+
+def tfd_matmul_relu_mask(a, b, bias, c, relu_mask, transpose_a=False, transpose_b=False, rounding="nearest",
+                         stream=None):
+    """c = Relu(op(a) @ op(b) + bias) and relu_mask = the bits of c > 0 (the
+    forward MatMul that also records its ReLU mask; see include/tfdense.h)."""
+    lda, ldb, ldc = _rowmajor(a, "a"), _rowmajor(b, "b"), _rowmajor(c, "c")
+    m = a.size(1) if transpose_a else a.size(0)
+    k = a.size(0) if transpose_a else a.size(1)
+    kb = b.size(1) if transpose_b else b.size(0)
+    n = b.size(0) if transpose_b else b.size(1)
+    if kb != k or tuple(c.shape) != (m, n):
+        raise ValueError(f"shape mismatch: op(a) {m}x{k}, op(b) {kb}x{n}, c {tuple(c.shape)}")
+    if b.dtype != a.dtype or c.dtype != a.dtype:
+        raise ValueError("a, b and c must have the same dtype")
+    if bias.dtype != torch.float32 or bias.numel() != n or not bias.is_contiguous():
+        raise ValueError("bias must be a contiguous fp32 vector of length n")
+    _mask(relu_mask, m, n)
+    _check(load().tfd_matmul_relu_mask(int(transpose_a), int(transpose_b), m, n, k, _ptr(a), lda, _ptr(b), ldb,
+                                       _ptr(bias), _ptr(c), ldc, _ptr(relu_mask), _dtype(a), ROUNDINGS[rounding],
+                                       _stream(stream)))
+    return c, relu_mask
+
+
+def tfd_relu_mask_grad_bias_add_grad(gradients, relu_mask, backprops, bias_grad, workspace=None, stream=None):
+    """tfd_relu_grad_bias_add_grad with the Relu test read from a ReLU mask."""
+    rows, cols = gradients.shape
+    _flat(gradients, "gradients")
+    _mask(relu_mask, rows, cols)
+    if backprops is not None:
+        _flat(backprops, "backprops")
+    need = tfd_reduction_workspace_size(rows, cols, gradients.dtype)
+    ws = _workspace(need, gradients.device, workspace)
+    _check(load().tfd_relu_mask_grad_bias_add_grad(_ptr(gradients), _ptr(relu_mask), _ptr(backprops),
+                                                   _ptr(bias_grad), rows, cols, _dtype(gradients), _ptr(ws),
+                                                   ws.numel(), _stream(stream)))
+    return backprops, bias_grad
+
+
+def tfd_matmul_relu_mask_grad_bias_add_grad(a, b, relu_mask, backprops, bias_grad, transpose_a=False,
+                                            transpose_b=False, rounding="nearest", workspace=None, stream=None):
+    """tfd_matmul_relu_grad_bias_add_grad with the Relu test read from a ReLU
+    mask of the m x n forward output (see include/tfdense.h)."""
+    lda, ldb = _rowmajor(a, "a"), _rowmajor(b, "b")
+    m = a.size(1) if transpose_a else a.size(0)
+    k = a.size(0) if transpose_a else a.size(1)
+    kb = b.size(1) if transpose_b else b.size(0)
+    n = b.size(0) if transpose_b else b.size(1)
+    if kb != k or tuple(backprops.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    if not backprops.is_contiguous() or backprops.dtype != a.dtype or b.dtype != a.dtype:
+        raise ValueError("backprops must be contiguous; a, b and backprops must share a dtype")
+    _mask(relu_mask, m, n)
+    if bias_grad.dtype != torch.float32 or bias_grad.numel() != n or not bias_grad.is_contiguous():
+        raise ValueError("bias_grad must be a contiguous fp32 vector of length n")
+    ws = _workspace(tfd_matmul_relu_grad_workspace_size(m, n, a.dtype), a.device, workspace)
+    _check(load().tfd_matmul_relu_mask_grad_bias_add_grad(int(transpose_a), int(transpose_b), m, n, k, _ptr(a), lda,
+                                                          _ptr(b), ldb, _ptr(relu_mask), _ptr(backprops),
+                                                          _ptr(bias_grad), _dtype(a), ROUNDINGS[rounding], _ptr(ws),
+                                                          ws.numel(), _stream(stream)))
     return backprops, bias_grad
 
 

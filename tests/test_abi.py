@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.tfd_abi_version() == 2
+    assert lib.tfd_abi_version() == 3
     assert lib.tfd_status_string(0) == b"ok"
     assert lib.tfd_status_string(1) == b"invalid argument"
     assert lib.tfd_status_string(2) == b"unsupported"
@@ -149,3 +149,55 @@ def test_fused_relu_grad_matmul_validation(lib):
     assert call(rounding=9) == 1
     assert call(bp=args["feat"] + 64) == 1 and b"overlap" in lib.tfd_last_error()
     assert call(n=0, feat=None, bp=None, db=None, ws=None, ws_bytes=0) == 0      # nothing to do
+
+
+def test_relu_mask_validation(lib):
+    rm = lib.tfd_relu_mask
+    assert rm(FAKE, FAKE * 2, -1, 32, 1, None) == 1
+    assert rm(FAKE, FAKE * 2, 4, 32, 7, None) == 1                    # unknown type
+    assert rm(None, None, 0, 32, 1, None) == 0                        # empty no-op
+    assert rm(FAKE, None, 4, 32, 1, None) == 1
+    assert rm(FAKE, FAKE + 8, 4, 32, 1, None) == 1 and b"overlap" in lib.tfd_last_error()
+    assert rm(FAKE, FAKE * 2 + 2, 4, 32, 1, None) == 1 and b"aligned" in lib.tfd_last_error()
+
+    mm = lib.tfd_matmul_relu_mask
+
+    def fwd(ta=0, tb=1, m=512, n=256, k=128, lda=128, ldb=128, bias=FAKE * 3, c=FAKE * 4, ldc=256,
+            mask=FAKE * 5, dtype=1, rounding=0):
+        return mm(ta, tb, m, n, k, FAKE, lda, FAKE * 2, ldb, bias, c, ldc, mask, dtype, rounding, None)
+
+    assert fwd(m=-1) == 1
+    assert fwd(ta=1, tb=1) == 2
+    assert fwd(ldc=255) == 1 and b"leading dimension" in lib.tfd_last_error()
+    assert fwd(mask=None) == 1
+    assert fwd(bias=None) == 1
+    assert fwd(mask=FAKE * 5 + 2) == 1 and b"aligned" in lib.tfd_last_error()
+    assert fwd(dtype=0, rounding=1) == 1 and b"16-bit" in lib.tfd_last_error()
+    assert fwd(mask=FAKE * 4 + 64) == 1 and b"overlap" in lib.tfd_last_error()    # mask inside c
+    assert fwd(m=0, c=None, mask=None, bias=None) == 0
+
+    need = lib.tfd_reduction_workspace_size(1000, 300, 1)
+    g = lib.tfd_relu_mask_grad_bias_add_grad
+    assert g(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, -1, 300, 1, FAKE * 5, need, None) == 1
+    assert g(FAKE, None, FAKE * 3, FAKE * 4, 1000, 300, 1, FAKE * 5, need, None) == 1
+    assert g(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 1000, 300, 1, FAKE * 5, need - 1, None) == 1
+    assert b"workspace" in lib.tfd_last_error()
+    assert g(FAKE, FAKE * 2, FAKE * 2 + 64, FAKE * 4, 1000, 300, 1, FAKE * 5, need, None) == 1   # backprops on mask
+    assert b"overlap" in lib.tfd_last_error()
+
+    f = lib.tfd_matmul_relu_mask_grad_bias_add_grad
+    wneed = lib.tfd_matmul_relu_grad_workspace_size(512, 256, 1)
+
+    def bwd(ta=0, tb=1, m=512, n=256, k=128, lda=128, ldb=128, mask=FAKE * 3, bp=FAKE * 4, db=FAKE * 5,
+            dtype=1, rounding=0, ws=FAKE * 6, ws_bytes=wneed):
+        return f(ta, tb, m, n, k, FAKE, lda, FAKE * 2, ldb, mask, bp, db, dtype, rounding, ws, ws_bytes, None)
+
+    assert bwd(m=-1) == 1
+    assert bwd(ta=1, tb=1) == 2
+    assert bwd(lda=64) == 1
+    assert bwd(ws_bytes=wneed - 1) == 1 and b"workspace" in lib.tfd_last_error()
+    assert bwd(mask=None) == 1
+    assert bwd(db=None) == 1
+    assert bwd(mask=FAKE * 3 + 1) == 1 and b"aligned" in lib.tfd_last_error()
+    assert bwd(bp=FAKE * 3 + 64) == 1 and b"overlap" in lib.tfd_last_error()
+    assert bwd(n=0, mask=None, bp=None, db=None, ws=None, ws_bytes=0) == 0

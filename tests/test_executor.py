@@ -49,11 +49,12 @@ def test_schedule_is_topological_and_complete():
     assert len({plan[1], plan[2], plan[4]}) == 3      # three independent successors of node 0
 
 
+@pytest.mark.parametrize("masks", [False, True])
 @pytest.mark.parametrize("fuse", [False, True])
 @pytest.mark.parametrize("name", sorted(workloads.WORKLOADS))
-def test_step_graph_orders_updates_after_reads(name, fuse):
+def test_step_graph_orders_updates_after_reads(name, fuse, masks):
     w = workloads.workload(name)
-    ops = op_graph(w, fuse)
+    ops = op_graph(w, fuse, masks)
     names = [o[0] for o in ops]
     deps = executor.transitive_reduction(executor.dependencies([_N(*o) for o in ops]))
     anc = _ancestors(deps)
@@ -89,6 +90,17 @@ def test_step_graph_orders_updates_after_reads(name, fuse):
     plan = dict(executor.schedule(deps, 3))
     for l in range(1, L + 1):
         assert plan[idx[f"dx{l}"]] != plan[idx[f"dw{l}"]]
+    # with masks, each Relu layer's ReluGrad reads the mask its forward op wrote
+    for l in range(L):
+        key = f"m{l}"
+        writers = [n for n, _, wr in ops if key in wr]
+        readers = [n for n, rd, _ in ops if key in rd]
+        if masks and w.relus[l]:
+            assert writers == [f"fwd{l + 1}"] and len(readers) == 1
+            assert idx[writers[0]] in anc[idx[readers[0]]]
+            assert readers[0] == dy_producer(l + 1)
+        else:
+            assert not writers and not readers
 
 
 def test_schedule_of_one_stream_is_program_order_for_the_step():

@@ -62,8 +62,8 @@ def _assert_within(got, want, allowed, what):
     assert e <= allowed, f"{what}: max|err| = {e:.3e} > allowed {allowed:.3e}"
 
 
-def _run_gpu(w, inp, fuse=True):
-    s = DenseStep(w, inp, fuse=fuse)
+def _run_gpu(w, inp, fuse=True, masks=None):
+    s = DenseStep(w, inp, fuse=fuse, masks=masks)
     s.run()
     torch.cuda.synchronize()
     return s
@@ -249,6 +249,34 @@ def test_fused_step_equals_unfused(name, batch, dims):
         assert float((a.biases[l] - b.biases[l]).abs().max()) <= w.lr * tol + 2.0 ** -23 * float(
             b.biases[l].abs().max()), f"b_{l + 1}"
     assert torch.equal(a.dx[0], b.dx[0])
+
+
+@pytest.mark.parametrize("fuse", [True, False])
+@pytest.mark.parametrize("name,batch,dims", [("wide4096x4-bf16", 512, (512, 768, 512, 256, 512)),
+                                             ("wide4096x4-bf16", 1032, (512, 768, 512, 256, 512)),
+                                             ("wide4096x4-bf16-trunc", 768, (256, 512, 256, 256, 512)),
+                                             ("tall512x32768-bf16", 512, (512, 1024)),
+                                             ("wide4096x4-f32", 520, (136, 256, 512, 264, 128)),
+                                             ("mlp784-1024-1024-10-xent", None, None)])
+def test_masked_step_equals_features_step(name, batch, dims, fuse):
+    """A step that keeps ReLU masks (one bit of H > 0 per element, written by
+    the forward MatMul) stores exactly what the features-based step stores:
+    every tensor, db included, bit for bit."""
+    w = workloads.workload(name)
+    if batch is not None:
+        w = w.scaled(batch=batch, dims=dims)
+    inp = workloads.generate(w, seed=6)
+    a = _run_gpu(w, inp, fuse=fuse, masks=True)
+    b = _run_gpu(w, inp, fuse=fuse, masks=False)
+    assert any(m is not None for m in a.masks) and all(m is None for m in b.masks)
+    for l in range(w.layers):
+        if a.masks[l] is not None:
+            want = oracle.relu_mask(to_f64(a.h[l + 1]))
+            assert np.array_equal(a.masks[l].cpu().numpy().view(np.uint32), want), f"mask_{l + 1}"
+    pairs = [(a.h[l + 1], b.h[l + 1]) for l in range(w.layers)] + [(a.dy_of(l), b.dy_of(l)) for l in range(w.layers)]
+    pairs += list(zip(a.dw + a.db + a.variables(), b.dw + b.db + b.variables())) + [(a.loss, b.loss), (a.dx[0], b.dx[0])]
+    for x, y in pairs:
+        assert torch.equal(x.view(torch.uint8), y.view(torch.uint8))
 
 
 @pytest.mark.parametrize("name", ["dense784x100", "mlp784-1024-1024-10-xent", "wide4096x4-bf16"])

@@ -137,6 +137,46 @@ def test_relu_grad_mask_is_strict():
     assert not np.any(np.signbit(oracle.relu_grad(-g, f)[1:4]))
 
 
+def test_relu_mask_worked_example():
+    # row 0: positives in columns 0, 5, 31 (word 0) and 32, 39 (word 1);
+    # row 1: only non-positive values, NaN and a subnormal positive in column 33
+    f = np.zeros((2, 40))
+    f[0, [0, 5, 31, 32, 39]] = [1.0, 2.0, 1e-30, 3.0, 7.0]
+    f[0, [1, 2, 33]] = [-1.0, -0.0, -5.0]
+    f[1, :] = -1.0
+    f[1, [3, 4, 5, 33]] = [0.0, -0.0, np.nan, 1e-40]
+    want = np.array([[0x80000021, 0x00000081], [0x00000000, 0x00000002]], dtype=np.uint32)
+    got = oracle.relu_mask(f)
+    assert got.dtype == np.uint32 and got.shape == (2, 2)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("cols", [1, 31, 32, 33, 100, 257])
+def test_relu_mask_unpacks_to_the_test_and_pads_with_zeros(cols):
+    rng = np.random.default_rng(cols)
+    f = rng.standard_normal((7, cols))
+    f[rng.random((7, cols)) < 0.1] = 0.0
+    w = oracle.relu_mask(f)
+    assert w.shape == (7, (cols + 31) // 32)
+    # little-endian bytes of each word, then bits least significant first
+    bits = np.unpackbits(w.astype("<u4").view(np.uint8), axis=1, bitorder="little")
+    assert np.array_equal(bits[:, :cols].astype(bool), f > 0)
+    assert not bits[:, cols:].any()
+    assert np.array_equal(bits.sum(axis=1), (f > 0).sum(axis=1))
+
+
+def test_relu_grad_from_mask_equals_relu_grad():
+    rng = np.random.default_rng(3)
+    for cols in (5, 32, 70):
+        g = rng.standard_normal((9, cols))
+        h = oracle.relu(rng.standard_normal((9, cols)))
+        h[0, :3] = [0.0, -0.0, 1e-45]
+        got = oracle.relu_grad_from_mask(g, oracle.relu_mask(h))
+        want = oracle.relu_grad(g, h)
+        assert np.array_equal(got, want)
+        assert not np.any(np.signbit(got[want == 0]))
+
+
 def test_bias_add_grad_exact_sums():
     rng = np.random.default_rng(1)
     g = rng.integers(-100, 101, size=(37, 9)).astype(np.float64)
