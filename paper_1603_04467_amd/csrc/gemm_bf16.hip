@@ -339,9 +339,11 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
           bits |= (bf16_bits_to_f32(v[e] & 0xFFFFu) > 0.0f ? 1u : 0u) << (2 * e);
           bits |= (bf16_bits_to_f32(v[e] >> 16) > 0.0f ? 1u : 0u) << (2 * e + 1);
         }
+        // OR over the 4 lanes of a quad with DPP quad permutations (lane ^ 1,
+        // then lane ^ 2), register to register
         uint32_t word = bits << (8 * (cc & 3));
-        word |= __shfl_xor(word, 1);
-        word |= __shfl_xor(word, 2);
+        word |= (uint32_t)__builtin_amdgcn_mov_dpp((int)word, 0xB1, 0xF, 0xF, false);
+        word |= (uint32_t)__builtin_amdgcn_mov_dpp((int)word, 0x4E, 0xF, 0xF, false);
         if ((cc & 3) == 0) p.mask_out[(int64_t)(m0 + row) * p.ldm + (n0 >> 5) + (cc >> 2)] = word;
       }
       *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc) = v;
