@@ -14,7 +14,8 @@
 //    values (512 B rows, chunks XOR-swizzled by k) and read with the gfx950
 //    transposing read ds_read_b64_tr_b16, which hands each lane of a 16-lane
 //    group four consecutive k of one column (two reads make the eight k an
-//    MFMA lane needs), so no transpose pass is needed anywhere;
+//    MFMA lane needs), so no transpose pass is needed anywhere (issued as
+//    inline assembly, see ds_read_tr16_b64);
 //  - fragments are double-buffered in registers: the reads for k-step q+1 are
 //    issued before the 16 MFMAs of k-step q.
 // K-slot assignment (identical for both operands, so each k is summed once):
@@ -33,9 +34,7 @@ namespace tfd {
 
 namespace {
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;
 
@@ -115,6 +114,22 @@ __device__ __forceinline__ int epi_off(int row, int col) {
   return row * 512 + (((col >> 3) ^ (((row >> 2) & 7) << 2)) << 4) + (col & 7) * 2;
 }
 
+// The transposing read ds_read_b64_tr_b16 is issued as inline assembly.
+// Through its builtin, the compiler's wait insertion treats it as an LDS
+// access that may overlap the global -> LDS copies in flight and puts a
+// vmcnt(0) before the first one of every k-tile: the copy of k-tile t+1 then
+// completes before k-step 0 of k-tile t has run, and hardly overlaps the
+// matrix work. As inline assembly it is not waited on; frag_wait() below
+// waits for it (lgkmcnt) and ties the fragment registers, so no instruction
+// that reads them can be scheduled before the wait.
+__device__ __forceinline__ uint2 ds_read_tr16_b64(const char* p) {
+  uint2 u;
+  const uint32_t addr = (uint32_t)(uintptr_t)((lds_void*)p);
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(u) : "v"(addr));
+  return u;
+}
+__device__ __forceinline__ void frag_wait(u32x4& f) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f)); }
+
 // Fragment of 32 rows (A) or 32 columns (B) starting at `base`, k-step q.
 template <bool KC>
 __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, int lane) {
@@ -132,8 +147,7 @@ __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, in
     for (int s = 0; s < 2; ++s) {
       const int kr = kb + 4 * s;
       const int off = kr * 512 + (((mn >> 3) ^ swz_mn(kr)) << 4) + (mn & 7) * 2;
-      const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + off));
-      const uint2 u = __builtin_bit_cast(uint2, v);
+      const uint2 u = ds_read_tr16_b64(tile + off);
       out[2 * s] = u.x;
       out[2 * s + 1] = u.y;
     }
@@ -207,6 +221,13 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int cb = q & 1, nb = cb ^ 1;
+      if constexpr (!A_KC || !B_KC) {
+        // this k-step's fragments include transposing (inline assembly) reads
+#pragma unroll
+        for (int i = 0; i < kFM; ++i) frag_wait(fa[cb][i]);
+#pragma unroll
+        for (int j = 0; j < kFN; ++j) frag_wait(fb[cb][j]);
+      }
       if (q < 3) {
 #pragma unroll
         for (int i = 0; i < kFM; ++i) fa[nb][i] = read_frag<A_KC>(st, wm * kWTM + i * 32, q + 1, lane);
