@@ -6,8 +6,8 @@ SGD update) through libtfdense on one MI355X.
 Prints ONE JSON line. The headline workload is the 4-layer, 4096-wide MLP
 with 16-bit activations/weights, fp32 accumulation and fp32 master weights,
 batch 16384 ("wide4096x4-bf16"); its fp32 twin at batch 8192
-("wide4096x4-f32") and the MNIST-shaped steps are timed in the same run and
-reported under "also".
+("wide4096x4-f32"), the truncating 16-bit variant, the tall 512 -> 32768 layer
+and the MNIST-shaped steps are timed in the same run and reported under "also".
 
 Timing: every step starts from the same Variables (a stream-ordered restore
 before the step's start event), so each timed step is exactly the computation
@@ -40,10 +40,11 @@ PRIMARY = "wide4096x4-bf16"
 # steps too small to fill the GPU with one kernel at a time: also timed with
 # concurrent streams and HIP graph replay
 LAUNCH_BOUND = ("mlp784-1024-1024-10-xent", "mlp784-1024-1024-10", "dense784x100")
-# timed in the same run and reported under "also": the fp32 twin, then the
-# MNIST-shaped steps (classifier head and squared-error head) and the single layer
-SECONDARY = ("wide4096x4-f32", "wide4096x4-bf16-trunc", "mlp784-1024-1024-10-xent", "mlp784-1024-1024-10",
-             "dense784x100")
+# timed in the same run and reported under "also": the fp32 twin, the truncating
+# 16-bit variant, the tall 512 -> 32768 layer (given upstream gradient, no update),
+# then the MNIST-shaped steps (classifier head and squared-error head) and the single layer
+SECONDARY = ("wide4096x4-f32", "wide4096x4-bf16-trunc", "tall512x32768-bf16", "mlp784-1024-1024-10-xent",
+             "mlp784-1024-1024-10", "dense784x100")
 
 
 def _gemm_bytes(shape, layout, eb):
@@ -127,7 +128,12 @@ def time_workload(name: str, steps: int, warmup: int):
             d.update(layout=lay, shape=[m, n, k], flops=f, tflops=f / (d["ms"] * 1e-3) / 1e12)
         elif kind == "relugrad":
             M = w.dims[l]
-            byt = (3 * N * M * eb if w.relus[l - 1] else N * M * eb) + 4 * M
+            if not w.relus[l - 1]:
+                byt = N * M * eb + 4 * M                 # BiasAddGrad alone
+            elif s.use_masks:
+                byt = 2 * N * M * eb + N * M // 8 + 4 * M  # gradient and 1-bit mask in, dY out
+            else:
+                byt = 3 * N * M * eb + 4 * M             # gradient and features in, dY out
             d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
         elif kind == "sgd":
             K, M = w.dims[l - 1], w.dims[l]
