@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TFD_ABI_VERSION 3
+#define TFD_ABI_VERSION 4
 
 #if defined(__GNUC__)
 #define TFD_API __attribute__((visibility("default")))
@@ -109,6 +109,27 @@ TFD_API tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64
                       const void* b, int64_t ldb, tfd_dtype b_type,
                       void* c, int64_t ldc, tfd_dtype c_type,
                       const float* bias, tfd_epilogue epilogue, void* stream);
+
+/*
+ * tfd_matmul with a caller-owned workspace. The contract (arguments, types,
+ * epilogue, rounding, errors) is tfd_matmul's. The workspace lets the library
+ * split the reduction over k across several workgroups per output tile when
+ * the output has too few 256 x 256 tiles to occupy every compute unit (16-bit
+ * operands, m and n multiples of 256, k a multiple of 64): each split writes
+ * fp32 partial sums to the workspace and a second kernel adds them in split
+ * order, applies the epilogue and rounds once. The result then differs from
+ * tfd_matmul's only in how the k sum is grouped, and is the same on every
+ * call. With a workspace smaller than tfd_matmul_workspace_size (or NULL),
+ * or one that overlaps an operand, the call is exactly tfd_matmul.
+ */
+TFD_API size_t tfd_matmul_workspace_size(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                         tfd_dtype a_type, tfd_dtype b_type, tfd_dtype c_type);
+TFD_API tfd_status tfd_matmul_with_workspace(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                             const void* a, int64_t lda, tfd_dtype a_type,
+                                             const void* b, int64_t ldb, tfd_dtype b_type,
+                                             void* c, int64_t ldc, tfd_dtype c_type,
+                                             const float* bias, tfd_epilogue epilogue,
+                                             void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * BiasAdd, the broadcast Add of Figure 1 on its own:

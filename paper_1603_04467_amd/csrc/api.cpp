@@ -62,42 +62,131 @@ const char* tfd_status_string(tfd_status s) {
 
 const char* tfd_last_error(void) { return g_err; }
 
+}  // extern "C"
+
+namespace {
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
+
+// The k split a 16-bit whole-tile problem would use, and its workspace bytes.
+int split_plan(const tfd::GemmDesc& d, int64_t* kt_per, size_t* bytes) {
+  *kt_per = 0;
+  *bytes = 0;
+  if (!tfd::gemm_bf16_256_ok(d) || tfd::gemm_tile_override() != 0) return 1;
+  int s = tfd::gemm_bf16_256_splits(d, device_cus());
+  if (s < 2) return 1;
+  const int64_t kt = d.k / 64;
+  const int64_t per = (kt + s - 1) / s;
+  s = (int)((kt + per - 1) / per);  // every split non-empty
+  if (s < 2) return 1;
+  *kt_per = per;
+  *bytes = (size_t)s * (size_t)d.m * (size_t)d.n * sizeof(float);
+  return s;
+}
+
+tfd_status matmul_impl(const char* fn, int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                       const void* a, int64_t lda, tfd_dtype a_type, const void* b, int64_t ldb, tfd_dtype b_type,
+                       void* c, int64_t ldc, tfd_dtype c_type, const float* bias, tfd_epilogue epilogue,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+}  // namespace
+
+extern "C" {
+
 tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
                       const void* a, int64_t lda, tfd_dtype a_type,
                       const void* b, int64_t ldb, tfd_dtype b_type,
                       void* c, int64_t ldc, tfd_dtype c_type,
                       const float* bias, tfd_epilogue epilogue, void* stream) {
+  return matmul_impl("tfd_matmul", transpose_a, transpose_b, m, n, k, a, lda, a_type, b, ldb, b_type, c, ldc, c_type,
+                     bias, epilogue, nullptr, 0, stream);
+}
+
+size_t tfd_matmul_workspace_size(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k, tfd_dtype a_type,
+                                 tfd_dtype b_type, tfd_dtype c_type) {
+  if (m <= 0 || n <= 0 || k <= 0 || !valid_dtype(a_type) || !valid_dtype(b_type) || !valid_dtype(c_type)) return 0;
+  if (transpose_a && transpose_b) return 0;
+  tfd::GemmDesc d;
+  d.ta = transpose_a != 0;
+  d.tb = transpose_b != 0;
+  d.m = m;
+  d.n = n;
+  d.k = k;
+  // the plan depends on the shape and types; contiguous, aligned operands are assumed
+  d.a = reinterpret_cast<const void*>(uintptr_t(256));
+  d.b = d.a;
+  d.c = reinterpret_cast<void*>(uintptr_t(256));
+  d.lda = transpose_a ? m : k;
+  d.ldb = transpose_b ? k : n;
+  d.ldc = n;
+  d.in_bf16 = a_type == TFD_BF16 && b_type == TFD_BF16;
+  d.out_bf16 = c_type == TFD_BF16;
+  d.bias = nullptr;
+  d.epi = 0;
+  int64_t per;
+  size_t bytes;
+  split_plan(d, &per, &bytes);
+  return bytes;
+}
+
+tfd_status tfd_matmul_with_workspace(int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                                     const void* a, int64_t lda, tfd_dtype a_type, const void* b, int64_t ldb,
+                                     tfd_dtype b_type, void* c, int64_t ldc, tfd_dtype c_type, const float* bias,
+                                     tfd_epilogue epilogue, void* workspace, size_t workspace_bytes, void* stream) {
+  return matmul_impl("tfd_matmul_with_workspace", transpose_a, transpose_b, m, n, k, a, lda, a_type, b, ldb, b_type,
+                     c, ldc, c_type, bias, epilogue, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+tfd_status matmul_impl(const char* fn, int transpose_a, int transpose_b, int64_t m, int64_t n, int64_t k,
+                       const void* a, int64_t lda, tfd_dtype a_type, const void* b, int64_t ldb, tfd_dtype b_type,
+                       void* c, int64_t ldc, tfd_dtype c_type, const float* bias, tfd_epilogue epilogue,
+                       void* workspace, size_t workspace_bytes, void* stream) {
   g_err[0] = 0;
-  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "tfd_matmul: negative size m=%lld n=%lld k=%lld", (long long)m, (long long)n, (long long)k);
+  if (m < 0 || n < 0 || k < 0) return fail(TFD_EINVAL, "%s: negative size m=%lld n=%lld k=%lld", fn, (long long)m, (long long)n, (long long)k);
   if (!valid_dtype(a_type) || !valid_dtype(b_type) || !valid_dtype(c_type))
-    return fail(TFD_EINVAL, "tfd_matmul: unknown element type");
+    return fail(TFD_EINVAL, "%s: unknown element type", fn);
   const bool trunc16 = ((int)epilogue & TFD_EPI_TRUNCATE_16) != 0;
   const int op = (int)epilogue & ~(int)TFD_EPI_TRUNCATE_16;
   if (op != TFD_EPI_NONE && op != TFD_EPI_BIAS && op != TFD_EPI_BIAS_RELU)
-    return fail(TFD_EINVAL, "tfd_matmul: unknown epilogue %d", (int)epilogue);
+    return fail(TFD_EINVAL, "%s: unknown epilogue %d", fn, (int)epilogue);
   if (trunc16 && c_type != TFD_BF16)
-    return fail(TFD_EINVAL, "tfd_matmul: TFD_EPI_TRUNCATE_16 needs a 16-bit output");
+    return fail(TFD_EINVAL, "%s: TFD_EPI_TRUNCATE_16 needs a 16-bit output", fn);
   if (transpose_a && transpose_b)
-    return fail(TFD_EUNSUPPORTED, "tfd_matmul: transpose_a and transpose_b together are not implemented");
+    return fail(TFD_EUNSUPPORTED, "%s: transpose_a and transpose_b together are not implemented", fn);
   if (a_type != b_type || (a_type == TFD_F32 && c_type != TFD_F32))
-    return fail(TFD_EUNSUPPORTED, "tfd_matmul: element types (a=%d, b=%d, c=%d) not implemented", a_type, b_type, c_type);
+    return fail(TFD_EUNSUPPORTED, "%s: element types (a=%d, b=%d, c=%d) not implemented", fn, a_type, b_type, c_type);
   // The kernels index with 32-bit tile coordinates.
   if (m > (1LL << 30) || n > (1LL << 30) || k > (1LL << 30))
-    return fail(TFD_EUNSUPPORTED, "tfd_matmul: dimension above 2^30");
+    return fail(TFD_EUNSUPPORTED, "%s: dimension above 2^30", fn);
   const int64_t a_rows = transpose_a ? k : m, a_cols = transpose_a ? m : k;
   const int64_t b_rows = transpose_b ? n : k, b_cols = transpose_b ? k : n;
   if (lda < (a_cols > 0 ? a_cols : 1) || ldb < (b_cols > 0 ? b_cols : 1) || ldc < (n > 0 ? n : 1))
-    return fail(TFD_EINVAL, "tfd_matmul: leading dimension smaller than the row (lda=%lld ldb=%lld ldc=%lld)", (long long)lda, (long long)ldb, (long long)ldc);
+    return fail(TFD_EINVAL, "%s: leading dimension smaller than the row (lda=%lld ldb=%lld ldc=%lld)", fn, (long long)lda, (long long)ldb, (long long)ldc);
   if (m == 0 || n == 0) return TFD_OK;
-  if (!c) return fail(TFD_EINVAL, "tfd_matmul: c is NULL");
-  if (k > 0 && (!a || !b)) return fail(TFD_EINVAL, "tfd_matmul: a or b is NULL");
-  if (op != TFD_EPI_NONE && !bias) return fail(TFD_EINVAL, "tfd_matmul: the bias epilogue needs a bias");
+  if (!c) return fail(TFD_EINVAL, "%s: c is NULL", fn);
+  if (k > 0 && (!a || !b)) return fail(TFD_EINVAL, "%s: a or b is NULL", fn);
+  if (op != TFD_EPI_NONE && !bias) return fail(TFD_EINVAL, "%s: the bias epilogue needs a bias", fn);
   const int ab = elem_bytes(a_type), cb = elem_bytes(c_type);
   const size_t c_span = span(m, n, ldc, cb);
   if (overlaps(c, c_span, a, span(a_rows, a_cols, lda, ab)) ||
       overlaps(c, c_span, b, span(b_rows, b_cols, ldb, ab)) ||
       (op != TFD_EPI_NONE && overlaps(c, c_span, bias, (size_t)n * 4)))
-    return fail(TFD_EINVAL, "tfd_matmul: c overlaps an input");
+    return fail(TFD_EINVAL, "%s: c overlaps an input", fn);
   tfd::GemmDesc d;
   d.ta = transpose_a != 0;
   d.tb = transpose_b != 0;
@@ -114,8 +203,37 @@ tfd_status tfd_matmul(int transpose_a, int transpose_b, int64_t m, int64_t n, in
   d.out_bf16 = c_type == TFD_BF16;
   d.bias = bias;
   d.epi = op | (trunc16 ? tfd::kEpiTrunc16 : 0);
-  return hip_status(tfd::launch_gemm(d, as_stream(stream)), "tfd_matmul launch");
+  hipStream_t st = as_stream(stream);
+  if (workspace) {
+    int64_t kt_per;
+    size_t need;
+    const int splits = split_plan(d, &kt_per, &need);
+    if (splits > 1 && workspace_bytes >= need && (reinterpret_cast<uintptr_t>(workspace) & 15) == 0 &&
+        !overlaps(workspace, need, a, span(a_rows, a_cols, lda, ab)) &&
+        !overlaps(workspace, need, b, span(b_rows, b_cols, ldb, ab)) && !overlaps(workspace, need, c, c_span) &&
+        !(op != TFD_EPI_NONE && overlaps(workspace, need, bias, (size_t)n * 4))) {
+      // the k range split over `splits` workgroups per tile: fp32 partial
+      // products in the workspace, then their ordered sum with the epilogue
+      tfd::GemmDesc g = d;
+      g.c = workspace;
+      g.ldc = n;
+      g.out_bf16 = false;
+      g.bias = nullptr;
+      g.epi = 0;
+      g.splits = splits;
+      g.kt_per = kt_per;
+      hipError_t e = tfd::launch_gemm_bf16_256(g, st);
+      if (e == hipSuccess) e = tfd::launch_splitk_reduce(static_cast<const float*>(workspace), splits, d, st);
+      return hip_status(e, "tfd_matmul launch");
+    }
+  }
+  return hip_status(tfd::launch_gemm(d, st), "tfd_matmul launch");
 }
+
+}  // namespace
+
+extern "C" {
+
 
 tfd_status tfd_bias_add(const void* value, const float* bias, void* out, int64_t rows, int64_t cols,
                         tfd_dtype type, void* stream) {

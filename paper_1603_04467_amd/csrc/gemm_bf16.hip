@@ -61,6 +61,11 @@ struct Params {
   const uint32_t* mask_in;   // ReluGrad epilogue from a mask instead of features
   uint32_t* mask_out;        // forward epilogue: bits of the stored output's > 0
   int64_t ldm;
+  // Split of the k range over `splits` workgroups per tile (1: none). Split
+  // s covers k-tiles [s * kt_per, min((s + 1) * kt_per, k / 64)) and writes
+  // its fp32 partial tile to c + s * m * ldc; the partials are summed by
+  // splitk_reduce_kernel.
+  int splits, kt_per;
 };
 
 // Epilogues of the whole-tile kernel beyond bias/ReLU (16-bit outputs only).
@@ -187,7 +192,13 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   constexpr int kWTM = kBM / kWavesM, kWTN = kBN / kWavesN;  // wave tile
   const int half = lane >> 5, l32 = lane & 31;
   int tm, tn;
-  tile_of_block(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
+  int bid = blockIdx.x, split = 0;
+  if (p.splits > 1) {
+    const int tiles = p.tiles_m * p.tiles_n;
+    split = bid / tiles;
+    bid -= split * tiles;
+  }
+  tile_of_block(bid, p.tiles_m, p.tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
 
   f32x16 acc[kFM][kFN];
@@ -198,9 +209,11 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int kt_count = p.k / kBK;
-  copy_tile<A_KC, kThreads>(p.a, p.lda, m0, 0, smem, wave, lane);
-  copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, 0, smem + kOperandBytes, wave, lane);
+  // this workgroup's k-tiles: kt0 .. kt0 + kt_count - 1
+  const int kt0 = split * p.kt_per;
+  const int kt_count = min(p.k / kBK - kt0, p.kt_per);
+  copy_tile<A_KC, kThreads>(p.a, p.lda, m0, kt0 * kBK, smem, wave, lane);
+  copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, kt0 * kBK, smem + kOperandBytes, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
   __syncthreads();
 
@@ -215,8 +228,8 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     char* nx = smem + ((kt + 1) & 1) * kStageBytes;
     const bool more = kt + 1 < kt_count;
     if (more) {
-      copy_tile<A_KC, kThreads>(p.a, p.lda, m0, (kt + 1) * kBK, nx, wave, lane);
-      copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, (kt + 1) * kBK, nx + kOperandBytes, wave, lane);
+      copy_tile<A_KC, kThreads>(p.a, p.lda, m0, (kt0 + kt + 1) * kBK, nx, wave, lane);
+      copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, (kt0 + kt + 1) * kBK, nx + kOperandBytes, wave, lane);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -403,7 +416,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     }
     return;
   } else {
-    OutT* C = static_cast<OutT*>(p.c);
+    OutT* C = static_cast<OutT*>(p.c) + (int64_t)split * p.m * p.ldc;
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
       const int col = n0 + wn * kWTN + j * 32 + l32;
@@ -447,8 +460,12 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.mask_in = d.mask_in;
   p.mask_out = d.mask_out;
   p.ldm = d.ldm;
-  dim3 grid(p.tiles_m * p.tiles_n), block(64 * WM * WN);
-  if (d.mask_in)
+  p.splits = d.splits > 1 ? d.splits : 1;
+  p.kt_per = p.splits > 1 ? (int)d.kt_per : p.k / kBK;
+  dim3 grid(p.tiles_m * p.tiles_n * p.splits), block(64 * WM * WN);
+  if (p.splits > 1)  // fp32 partial tiles, plain (the reduction applies the epilogue)
+    hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float, WM, WN>), grid, block, 0, s, p);
+  else if (d.mask_in)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpReluGradBits>), grid, block, 0, s, p);
   else if (d.mask_out)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, bf16, WM, WN, kEpMaskOut>), grid, block, 0, s, p);
@@ -482,6 +499,63 @@ int waves_for(const char* layout, int dflt) {
 }
 
 }  // namespace
+
+namespace {
+
+// Sum of the fp32 partial tiles of a split k range, in split order, then
+// the epilogue (bias, ReLU) and the single rounding to the output type. One
+// thread per 4 consecutive columns of a row.
+template <typename OutT>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits, int64_t m,
+                                                            int64_t n, OutT* __restrict__ c, int64_t ldc,
+                                                            const float* __restrict__ bias, int epi) {
+  const int64_t groups = n / 4;
+  const int64_t total = m * groups;
+  const int op = epi & kEpiOpMask;
+  const bool trunc16 = (epi & kEpiTrunc16) != 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t r = i / groups, c4 = (i - r * groups) * 4;
+    f32x4 v = *reinterpret_cast<const f32x4*>(ws + r * n + c4);
+    for (int sp = 1; sp < splits; ++sp) {
+      const f32x4 w = *reinterpret_cast<const f32x4*>(ws + ((int64_t)sp * m + r) * n + c4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += w[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float x = v[e];
+      if (op != 0) x += bias[c4 + e];
+      if (op == 2) x = relu_f32(x);
+      store_from_f32(c + r * ldc + c4 + e, x, trunc16);
+    }
+  }
+}
+
+}  // namespace
+
+int gemm_bf16_256_splits(const GemmDesc& d, int cus) {
+  // split the k range when the output has fewer whole tiles than compute
+  // units, keeping at least 8 k-tiles per split
+  const int64_t tiles = (d.m / kBM) * (d.n / kBN);
+  const int64_t kt = d.k / kBK;
+  if (tiles <= 0 || tiles >= cus || d.n % 4 != 0) return 1;
+  int64_t s = (cus + tiles - 1) / tiles;
+  if (s > kt / 8) s = kt / 8;
+  return s >= 2 ? (int)s : 1;
+}
+
+hipError_t launch_splitk_reduce(const float* ws, int splits, const GemmDesc& d, hipStream_t s) {
+  const int64_t total = d.m * (d.n / 4);
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (d.out_bf16)
+    hipLaunchKernelGGL((splitk_reduce_kernel<bf16>), (unsigned)blocks, 256, 0, s, ws, splits, d.m, d.n,
+                       static_cast<bf16*>(d.c), d.ldc, d.bias, d.epi);
+  else
+    hipLaunchKernelGGL((splitk_reduce_kernel<float>), (unsigned)blocks, 256, 0, s, ws, splits, d.m, d.n,
+                       static_cast<float*>(d.c), d.ldc, d.bias, d.epi);
+  return hipGetLastError();
+}
 
 bool gemm_bf16_256_ok(const GemmDesc& d) {
   // a 16-bit C leaves in 16-byte row chunks (and so do ReluGrad features in)

@@ -40,6 +40,11 @@ struct GemmDesc {
   const uint32_t* mask_in = nullptr;
   uint32_t* mask_out = nullptr;
   int64_t ldm = 0;
+  // Split of the k range (16-bit whole-tile kernel only): `splits`
+  // workgroups per output tile, kt_per 64-wide k-tiles each; c then receives
+  // `splits` fp32 partial matrices (ldc = n), summed by launch_splitk_reduce.
+  int splits = 1;
+  int64_t kt_per = 0;
 };
 
 constexpr int kEpiOpMask = 3;
@@ -52,6 +57,12 @@ int gemm_tile_override();
 // 16-bit operands, whole 256 x 256 tiles, k a multiple of 64 (gemm_bf16.hip).
 bool gemm_bf16_256_ok(const GemmDesc& d);
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s);
+// Number of k splits worth using for a whole-tile 16-bit problem on `cus`
+// compute units (1: none).
+int gemm_bf16_256_splits(const GemmDesc& d, int cus);
+// c = epilogue(sum of the `splits` fp32 partials in ws, in order), rounded once (d: the
+// original problem: c, ldc, out type, bias, epi).
+hipError_t launch_splitk_reduce(const float* ws, int splits, const GemmDesc& d, hipStream_t s);
 // fp32 problems too small to fill the GPU with 128 x 128 tiles (gemm_small.hip).
 bool gemm_small_preferred(const GemmDesc& d);
 hipError_t launch_gemm_small_f32(const GemmDesc& d, hipStream_t s);

@@ -85,7 +85,9 @@ def op_graph(w: Workload, fuse: bool = True, masks: bool = False):
             ops.append((f"dx{l + 1}", (dykey, f"W{l}", f"m{l - 1}" if mk(l - 1) else f"h{l}"),
                         (f"dy{l - 1}", f"db{l - 1}", "ws")))
         else:
-            ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}",)))
+            # the plain input-gradient MatMul may split its k range through the
+            # shared workspace
+            ops.append((f"dx{l + 1}", (dykey, f"W{l}"), (f"dx{l}", "ws")))
         ops.append((f"dw{l + 1}", (f"h{l}", dykey), (f"dw{l}",)))
         if w.update:
             ops.append((f"sgd{l + 1}", (f"dw{l}", f"db{l}"), (f"W{l}", f"b{l}")))
@@ -139,6 +141,8 @@ class DenseStep:
         need.append(T.tfd_softmax_xent_workspace_size(N))
         need += [T.tfd_matmul_relu_grad_workspace_size(N, w.dims[l], self.act) for l in range(1, L)]
         need.append(T.tfd_matmul_l2_loss_grad_workspace_size(N, w.dims[-1], self.act))
+        need += [T.tfd_matmul_workspace_size(N, w.dims[l], w.dims[l + 1], self.act, self.act, transpose_b=True)
+                 for l in range(L)]
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
         if self.weights_t is not None:
@@ -231,7 +235,8 @@ class DenseStep:
                                                          transpose_b=True, rounding=w.rounding, workspace=ws,
                                                          stream=st)
                 else:
-                    T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding, stream=st)
+                    T.tfd_matmul(dyl, self.weights[l], self.dx[l], transpose_b=True, rounding=w.rounding, workspace=ws,
+                                 stream=st)
 
             def dw(st):
                 T.tfd_matmul(self.h[l], dyl, self.dw[l], transpose_a=True, stream=st)

@@ -37,7 +37,7 @@ EXPORTS = (
     "tfd_softmax_xent_workspace_size", "tfd_softmax_cross_entropy_grad", "tfd_apply_gradient_descent",
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
     "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
-    "tfd_matmul_relu_mask_grad_bias_add_grad",
+    "tfd_matmul_relu_mask_grad_bias_add_grad", "tfd_matmul_workspace_size", "tfd_matmul_with_workspace",
 )
 
 
@@ -86,6 +86,9 @@ def load() -> ctypes.CDLL:
         "tfd_convert_f32_to_bf16": ([vp, vp, i64, i32, vp], i32),
         "tfd_convert_bf16_to_f32": ([vp, vp, i64, vp], i32),
         "tfd_relu_mask": ([vp, vp, i64, i64, i32, vp], i32),
+        "tfd_matmul_workspace_size": ([i32, i32, i64, i64, i64, i32, i32, i32], sz),
+        "tfd_matmul_with_workspace": ([i32, i32, i64, i64, i64, vp, i64, i32, vp, i64, i32, vp, i64, i32, vp, i32, vp, sz,
+                                       vp], i32),
         "tfd_matmul_relu_mask": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, vp, i32, i32, vp], i32),
         "tfd_relu_mask_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
         "tfd_matmul_relu_mask_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32,
@@ -142,10 +145,19 @@ def tfd_abi_version() -> int:
     return load().tfd_abi_version()
 
 
+def tfd_matmul_workspace_size(m, n, k, a_dtype, c_dtype, transpose_a=False, transpose_b=False) -> int:
+    """Workspace bytes that let tfd_matmul split the k range (0: no split)."""
+    td = lambda d: TFD_BF16 if d == torch.bfloat16 else TFD_F32  # noqa: E731
+    return load().tfd_matmul_workspace_size(int(transpose_a), int(transpose_b), m, n, k, td(a_dtype), td(a_dtype),
+                                            td(c_dtype))
+
+
 def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogue="none", rounding="nearest",
-               stream=None):
+               workspace=None, stream=None):
     """c = epilogue(op(a) @ op(b)) (see include/tfdense.h); rounding="truncate"
-    writes a 16-bit c with the truncating converter."""
+    writes a 16-bit c with the truncating converter. With a `workspace`
+    (uint8 device tensor) the call is tfd_matmul_with_workspace, which may
+    split the k range of an under-filled problem."""
     lda, ldb, ldc = _rowmajor(a, "a"), _rowmajor(b, "b"), _rowmajor(c, "c")
     m = a.size(1) if transpose_a else a.size(0)
     k = a.size(0) if transpose_a else a.size(1)
@@ -155,10 +167,16 @@ def tfd_matmul(a, b, c, transpose_a=False, transpose_b=False, bias=None, epilogu
         raise ValueError(f"shape mismatch: op(a) {m}x{k}, op(b) {kb}x{n}, c {tuple(c.shape)}")
     if bias is not None and (bias.dtype != torch.float32 or bias.numel() != n or not bias.is_contiguous()):
         raise ValueError("bias must be a contiguous fp32 vector of length n")
-    _check(load().tfd_matmul(int(transpose_a), int(transpose_b), m, n, k,
-                             _ptr(a), lda, _dtype(a), _ptr(b), ldb, _dtype(b), _ptr(c), ldc, _dtype(c),
-                             _ptr(bias), EPILOGUES[epilogue] | (TFD_EPI_TRUNCATE_16 if ROUNDINGS[rounding] else 0),
-                             _stream(stream)))
+    epi = EPILOGUES[epilogue] | (TFD_EPI_TRUNCATE_16 if ROUNDINGS[rounding] else 0)
+    if workspace is None:
+        _check(load().tfd_matmul(int(transpose_a), int(transpose_b), m, n, k,
+                                 _ptr(a), lda, _dtype(a), _ptr(b), ldb, _dtype(b), _ptr(c), ldc, _dtype(c),
+                                 _ptr(bias), epi, _stream(stream)))
+    else:
+        _check(load().tfd_matmul_with_workspace(int(transpose_a), int(transpose_b), m, n, k,
+                                                _ptr(a), lda, _dtype(a), _ptr(b), ldb, _dtype(b), _ptr(c), ldc,
+                                                _dtype(c), _ptr(bias), epi, _ptr(workspace), workspace.numel(),
+                                                _stream(stream)))
     return c
 
 

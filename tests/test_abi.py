@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.tfd_abi_version() == 3
+    assert lib.tfd_abi_version() == 4
     assert lib.tfd_status_string(0) == b"ok"
     assert lib.tfd_status_string(1) == b"invalid argument"
     assert lib.tfd_status_string(2) == b"unsupported"
@@ -201,3 +201,24 @@ def test_relu_mask_validation(lib):
     assert bwd(mask=FAKE * 3 + 1) == 1 and b"aligned" in lib.tfd_last_error()
     assert bwd(bp=FAKE * 3 + 64) == 1 and b"overlap" in lib.tfd_last_error()
     assert bwd(n=0, mask=None, bp=None, db=None, ws=None, ws_bytes=0) == 0
+
+
+def test_matmul_with_workspace_validation_and_plan(lib):
+    ws = lib.tfd_matmul_workspace_size
+    # 16-bit, 2 x 64 = 128 output tiles of 256 x 256 and 512 k-tiles: split in two
+    assert ws(0, 1, 16384, 512, 32768, 1, 1, 1) == 2 * 16384 * 512 * 4
+    assert ws(0, 1, 16384, 512, 32768, 1, 1, 0) == 2 * 16384 * 512 * 4
+    assert ws(0, 1, 16384, 4096, 4096, 1, 1, 1) == 0       # 1024 tiles: no split
+    assert ws(0, 1, 512, 512, 512, 1, 1, 1) == 0           # 8 k-tiles: too short to split
+    assert ws(0, 1, 2048, 512, 32768, 0, 0, 0) == 0        # fp32: no split
+    assert ws(0, 1, 300, 512, 32768, 1, 1, 1) == 0         # not whole tiles
+    assert ws(1, 1, 2048, 512, 32768, 1, 1, 1) == 0
+    assert ws(0, 1, -1, 512, 32768, 1, 1, 1) == 0
+    mw = lib.tfd_matmul_with_workspace
+    assert mw(0, 0, -1, 2, 3, FAKE, 3, 0, FAKE, 2, 0, FAKE * 4, 2, 0, None, 0, FAKE * 8, 64, None) == 1
+    assert lib.tfd_last_error().startswith(b"tfd_matmul_with_workspace: negative")
+    assert mw(0, 0, 4, 4, 8, FAKE, 7, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 0, FAKE * 8, 64, None) == 1
+    assert b"leading dimension" in lib.tfd_last_error()
+    assert mw(1, 1, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 0, FAKE * 8, 64, None) == 2
+    assert mw(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE + 16, 4, 0, None, 0, FAKE * 8, 64, None) == 1
+    assert mw(0, 0, 0, 4, 4, None, 4, 0, None, 4, 0, None, 4, 0, None, 0, None, 0, None) == 0
