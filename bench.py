@@ -104,6 +104,7 @@ def time_workload(name: str, steps: int, warmup: int):
         for (tag, e0), (_, e1) in zip(marks[:-1], marks[1:]):
             per_op.setdefault(tag, []).append(e0.elapsed_time(e1))
     ms = float(np.mean(step_ms))
+    pct = {f"p{q}": round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)}
     flops = w.flops()
     tflops = flops / (ms * 1e-3) / 1e12
 
@@ -163,6 +164,7 @@ def time_workload(name: str, steps: int, warmup: int):
     return {
         "workload": w,
         "ms": ms,
+        "ms_percentiles": pct,
         "wall_ms": wall,
         "tflops": tflops,
         "pct_peak": 100.0 * tflops / peak,
@@ -368,6 +370,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(r["ms"], 4),
+        "ms_per_step_percentiles": r["ms_percentiles"],
         "wall_ms_per_step": round(r["wall_ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -400,6 +403,7 @@ def main():
                 "value": round(r2["tflops"], 3),
                 "unit": "TFLOP/s",
                 "ms_per_step": round(r2["ms"], 4),
+                "ms_per_step_percentiles": r2["ms_percentiles"],
                 "pct_mfma_peak": round(r2["pct_peak"], 2),
                 "roofline": r2["roofline"],
                 "per_op": _per_op(r2["ops"]),
