@@ -160,6 +160,14 @@ __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, in
   }
 }
 
+// Outputs leave with the non-temporal hint (here and in the fp32 epilogue):
+// this kernel never re-reads them, and without the hint the dirty lines of
+// the output (1 GiB for a 16384 x 32768 layer) fill L2 and are written back
+// while the next tiles' operand panels are being fetched through it.
+__device__ __forceinline__ void store_stream(void* p, const u32x4& v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
 // Scheduling hint: 16 MFMAs spread evenly over kReads groups, each followed
 // by one LDS read.
 template <int T, int kReads, int kMfma>
@@ -339,7 +347,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
           cs[2 * e] += bf16_bits_to_f32(g0);
           cs[2 * e + 1] += bf16_bits_to_f32(g1);
         }
-        *reinterpret_cast<u32x4*>(p.grad + at) = g;
+        store_stream(p.grad + at, g);
       }
       if constexpr (EP == kEpReluGrad) {
         // ReluGrad: keep the value where the stored feature is > 0, +0
@@ -380,7 +388,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
         word |= (uint32_t)__builtin_amdgcn_mov_dpp((int)word, 0x4E, 0xF, 0xF, false);
         if ((cc & 3) == 0) p.mask_out[(int64_t)(m0 + row) * p.ldm + (n0 >> 5) + (cc >> 2)] = word;
       }
-      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc) = v;
+      store_stream(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc, v);
     }
     if constexpr (EP == kEpReluGrad || EP == kEpReluGradBits || EP == kEpLoss) {
       // column sums: each thread's rows, then the kRowStep threads of a
@@ -428,7 +436,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
           const int row = m0 + wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
           float v = acc[i][j][r] + bv;
           if (op == 2) v = relu_f32(v);
-          C[(int64_t)row * p.ldc + col] = v;
+          __builtin_nontemporal_store(v, &C[(int64_t)row * p.ldc + col]);
         }
       }
     }
