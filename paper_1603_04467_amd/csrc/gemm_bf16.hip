@@ -27,6 +27,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -168,6 +170,23 @@ __device__ __forceinline__ void store_stream(void* p, const u32x4& v) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
 }
 
+// v_writelane_b32 through its LLVM intrinsic (the compiler offers no
+// builtin for it): `old` with lane `lane` set to the wave-uniform `value`.
+extern "C" __device__ int tfd_writelane(int value, int lane, int old) __asm("llvm.amdgcn.writelane");
+
+// Two fp32 values as one word of 16-bit patterns (lo in the low half). The
+// nearest-even pair is one v_cvt_pk_bf16_f32 (a vector conversion; two
+// scalar ones would be two conversions and an OR).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+template <bool kTrunc>
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  if constexpr (kTrunc)
+    return (uint32_t)bf16_bits_trunc(lo) | ((uint32_t)bf16_bits_trunc(hi) << 16);
+  else
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
 // Scheduling hint: 16 MFMAs spread evenly over kReads groups, each followed
 // by one LDS read.
 template <int T, int kReads, int kMfma>
@@ -208,6 +227,23 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   }
   tile_of_block(bid, p.tiles_m, p.tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
+  // The epilogue op: fixed by the fused epilogues (mask out: bias + ReLU;
+  // squared error: bias; ReluGrad: none), else read from p.epi. The bias
+  // values of this lane's columns are fetched before the k loop so that
+  // their latency hides behind the first copies (with 4 waves, whose 256
+  // accumulators per lane leave no registers to spare, in the epilogue).
+  constexpr int kFixedOp = EP == kEpMaskOut                             ? 2
+                           : EP == kEpLoss                              ? 1
+                           : (EP == kEpReluGrad || EP == kEpReluGradBits) ? 0
+                                                                          : -1;
+  const int op = kFixedOp >= 0 ? kFixedOp : (p.epi & kEpiOpMask);
+  constexpr bool kEarlyBias = kWavesM * kWavesN >= 8;
+  float bias_v[kFN];
+  auto load_bias = [&]() {
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) bias_v[j] = op != 0 ? p.bias[n0 + wn * kWTN + j * 32 + l32] : 0.0f;
+  };
+  if constexpr (kEarlyBias) load_bias();
 
   f32x16 acc[kFM][kFN];
 #pragma unroll
@@ -278,8 +314,8 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     }
   }
 
+  if constexpr (!kEarlyBias) load_bias();
   const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
-  const int op = p.epi & kEpiOpMask;
   if constexpr (sizeof(OutT) == 2) {
     // 16-bit output: the rounded tile goes through LDS (row-major, 16-byte
     // chunks XOR-swizzled so that both the fragment-layout writes and the
@@ -308,19 +344,82 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     }
     __syncthreads();
     char* tile = smem;  // 256 rows x 512 bytes
+    // Staging. Accumulator registers r, r + 1 (r even) of a lane are rows R,
+    // R + 1 of its column: one packed conversion rounds both, and the two
+    // halves go to LDS as 16-bit writes. The epilogue op and the rounding
+    // are uniform, so they select one of six copies of this loop instead of
+    // being tested per element.
+    //
+    // With kEpMaskOut the ReLU mask comes from wave ballots of the rounded
+    // values: the 64 lanes of a staging step hold 32 consecutive columns of
+    // rows R (lanes 0-31) and R + 4 (lanes 32-63), so the ballot of "16-bit
+    // value > 0" over one half of the packed words is the two rows' mask
+    // words. They are gathered into registers (row rho of the wave tile,
+    // column word j: register rho / kRowsPerReg, lane kFN (rho % kRowsPerReg)
+    // + j) and stored after the staging.
+    constexpr int kRowsPerReg = 64 / kFN;
+    uint32_t mk[EP == kEpMaskOut ? kWTM / kRowsPerReg : 1];
 #pragma unroll
-    for (int j = 0; j < kFN; ++j) {
-      const int col = wn * kWTN + j * 32 + l32;
-      const float bv = op != 0 ? p.bias[n0 + col] : 0.0f;
+    for (int e = 0; e < (int)(sizeof(mk) / sizeof(mk[0])); ++e) mk[e] = 0;
+    auto stage = [&](auto op_tag, auto trunc_tag) {
+      constexpr int kOp = decltype(op_tag)::value;
+      constexpr bool kTrunc = decltype(trunc_tag)::value;
 #pragma unroll
-      for (int i = 0; i < kFM; ++i) {
+      for (int j = 0; j < kFN; ++j) {
+        const int col = wn * kWTN + j * 32 + l32;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * kWTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          float v = acc[i][j][r] + bv;
-          if (op == 2) v = relu_f32(v);
-          *reinterpret_cast<uint16_t*>(tile + epi_off(row, col)) = bf16_bits_mode(v, trunc16);
+        for (int i = 0; i < kFM; ++i) {
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const int q = i * 32 + 8 * (r >> 2) + (r & 3);  // wave-tile row R - 4 half
+            const int row = wm * kWTM + q + 4 * half;
+            float v0 = acc[i][j][r], v1 = acc[i][j][r + 1];
+            if constexpr (kOp != 0) {
+              v0 += bias_v[j];
+              v1 += bias_v[j];
+            }
+            if constexpr (kOp == 2) {
+              v0 = relu_f32(v0);
+              v1 = relu_f32(v1);
+            }
+            const uint32_t w = pack_bf16x2<kTrunc>(v0, v1);
+            *reinterpret_cast<uint16_t*>(tile + epi_off(row, col)) = (uint16_t)w;
+            *reinterpret_cast<uint16_t*>(tile + epi_off(row + 1, col)) = (uint16_t)(w >> 16);
+            if constexpr (EP == kEpMaskOut) {
+              const uint64_t b0 = __builtin_amdgcn_ballot_w64((int16_t)(w & 0xFFFFu) > 0);  // rows R, R + 4
+              const uint64_t b1 = __builtin_amdgcn_ballot_w64((int16_t)(w >> 16) > 0);      // rows R + 1, R + 5
+              const uint32_t words[4] = {(uint32_t)b0, (uint32_t)b1, (uint32_t)(b0 >> 32), (uint32_t)(b1 >> 32)};
+              constexpr int kDq[4] = {0, 1, 4, 5};
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const int rho = q + kDq[t];
+                mk[rho / kRowsPerReg] =
+                    (uint32_t)tfd_writelane((int)words[t], kFN * (rho % kRowsPerReg) + j, (int)mk[rho / kRowsPerReg]);
+              }
+            }
+          }
         }
+      }
+    };
+    auto stage_op = [&](auto op_tag) {
+      if (trunc16)
+        stage(op_tag, std::true_type{});
+      else
+        stage(op_tag, std::false_type{});
+    };
+    if constexpr (kFixedOp >= 0)
+      stage_op(std::integral_constant<int, kFixedOp>{});
+    else if (op == 2)
+      stage_op(std::integral_constant<int, 2>{});
+    else if (op == 1)
+      stage_op(std::integral_constant<int, 1>{});
+    else
+      stage_op(std::integral_constant<int, 0>{});
+    if constexpr (EP == kEpMaskOut) {
+#pragma unroll
+      for (int e = 0; e < kWTM / kRowsPerReg; ++e) {
+        const int rho = e * kRowsPerReg + lane / kFN;
+        p.mask_out[(int64_t)(m0 + wm * kWTM + rho) * p.ldm + ((n0 + wn * kWTN) >> 5) + lane % kFN] = mk[e];
       }
     }
     __syncthreads();
@@ -373,21 +472,6 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
           cs[2 * e + 1] += bf16_bits_to_f32(hi >> 16);
         }
       }
-      if constexpr (EP == kEpMaskOut) {
-        // 8 bits of this chunk, gathered into one word per 4 neighbouring lanes
-        uint32_t bits = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bits |= (bf16_bits_to_f32(v[e] & 0xFFFFu) > 0.0f ? 1u : 0u) << (2 * e);
-          bits |= (bf16_bits_to_f32(v[e] >> 16) > 0.0f ? 1u : 0u) << (2 * e + 1);
-        }
-        // OR over the 4 lanes of a quad with DPP quad permutations (lane ^ 1,
-        // then lane ^ 2), register to register
-        uint32_t word = bits << (8 * (cc & 3));
-        word |= (uint32_t)__builtin_amdgcn_mov_dpp((int)word, 0xB1, 0xF, 0xF, false);
-        word |= (uint32_t)__builtin_amdgcn_mov_dpp((int)word, 0x4E, 0xF, 0xF, false);
-        if ((cc & 3) == 0) p.mask_out[(int64_t)(m0 + row) * p.ldm + (n0 >> 5) + (cc >> 2)] = word;
-      }
       store_stream(static_cast<uint16_t*>(p.c) + (int64_t)(m0 + row) * p.ldc + n0 + 8 * cc, v);
     }
     if constexpr (EP == kEpReluGrad || EP == kEpReluGradBits || EP == kEpLoss) {
@@ -428,7 +512,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
       const int col = n0 + wn * kWTN + j * 32 + l32;
-      const float bv = op != 0 ? p.bias[col] : 0.0f;
+      const float bv = bias_v[j];
 #pragma unroll
       for (int i = 0; i < kFM; ++i) {
 #pragma unroll
