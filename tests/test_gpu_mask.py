@@ -164,3 +164,38 @@ def test_matmul_relu_mask_grad_bias_add_grad(m, n, k, layout, dt, rounding, wave
     dy = to_f64(bp)
     D = max(m, 1) * max(amax(dy), 1e-30)
     assert_close(to_f64(db), oracle.bias_add_grad(dy), D, TAU["f32"], "fused BiasAddGrad")
+
+
+@pytest.mark.parametrize("rounding", ["nearest", "truncate"])
+def test_mask_out_at_the_rounding_boundary(rounding):
+    """Outputs around the smallest 16-bit magnitudes (2^-134 .. 2^-131, fp32
+    denormals): which of them round to +0 depends on the rounding mode, and
+    the mask written beside the output must be exactly "stored value > 0".
+    C[r, c] = a_r b_c from one nonzero k per row; the products are exact in
+    fp32. Whether the matrix cores keep fp32 denormals is not asserted: each
+    stored value must be the oracle's rounding of the exact product, or +0."""
+    m = n = 256
+    k = 64
+    r = np.arange(m)
+    a_h = np.zeros((m, k))
+    a_h[:, 0] = 2.0 ** -70 * (1 + (r % 128) / 128)           # exact in 16 bits
+    c = np.arange(n)
+    s = (1 + (c % 64) / 64) * np.where(c % 3 == 0, -1.0, 1.0) * 2.0 ** ((c // 64) % 3 - 1)
+    b_h = np.zeros((n, k))                                   # B stored n x k (NT)
+    b_h[:, 0] = 2.0 ** -64 * s
+    a = torch.from_numpy(to_bf16_bits(a_h.astype(np.float32)).view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    b = torch.from_numpy(to_bf16_bits(b_h.astype(np.float32)).view(np.int16).copy()).view(torch.bfloat16).to(DEV)
+    assert np.array_equal(oracle.bf16_bits_to_f64(to_bf16_bits(a_h.astype(np.float32))), a_h)
+    assert np.array_equal(oracle.bf16_bits_to_f64(to_bf16_bits(b_h.astype(np.float32))), b_h)
+    bias = torch.zeros(n, device=DEV)
+    out = torch.full((m, n), float("nan"), dtype=torch.bfloat16, device=DEV)
+    mask = _mask_buf(m, n)
+    T.tfd_matmul_relu_mask(a, b, bias, out, mask, transpose_b=True, rounding=rounding)
+    torch.cuda.synchronize()
+    got = to_f64(out)
+    assert np.array_equal(_words(mask), oracle.relu_mask(got)), "mask differs from the stored output's > 0"
+    exact = np.maximum(np.outer(a_h[:, 0], b_h[:, 0]), 0.0)
+    want = oracle.round_to(exact, "bf16t" if rounding == "truncate" else "bf16")
+    assert np.all((got == want) | (got == 0.0)), "stored value is neither the rounded product nor +0"
+    # the case is not vacuous: products on both sides of the rounding boundary
+    assert np.any(want > 0) and np.any((exact > 0) & (want == 0))
