@@ -170,7 +170,13 @@ class DenseStep:
 
     def nodes(self):
         """The step's op nodes in program order (op_graph), each with the
-        launch of its kernels on a given stream."""
+        launch of its kernels on a given stream (built once: the buffers they
+        launch on are fixed at construction)."""
+        if "_nodes" not in self.__dict__:
+            self._nodes = self._build_nodes()
+        return self._nodes
+
+    def _build_nodes(self):
         from .executor import Node
 
         w, L = self.w, self.w.layers
