@@ -113,9 +113,10 @@ class DenseStep:
         # With fp32 masters, the 16-bit weights are kept twice: W [fan_in, fan_out]
         # for the input-gradient MatMul and W^T [fan_out, fan_in] so that the
         # forward MatMul reads its weight operand k-contiguous (transpose_b).
-        # Both copies are refreshed by the update kernel.
+        # Both copies are refreshed by the update kernel. 16-bit weights that
+        # are never updated (a given layer) get the same transposed copy once.
         self.weights_t = None
-        if self.masters is not None:
+        if self.masters is not None or (w.act == "bf16" and not w.update):
             self.weights_t = [torch.empty(w.dims[l + 1], w.dims[l], dtype=self.act, device=dev) for l in range(L)]
         # layout of the forward MatMul ("NN": H W; "NT": H (W^T)^T)
         self.forward_layout = "NT" if self.weights_t is not None else "NN"
@@ -146,11 +147,18 @@ class DenseStep:
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
         if self.weights_t is not None:
-            # derive W^T from the masters with the update kernel (alpha = 0)
+            # derive W^T with the update kernel (alpha = 0) from the masters, or
+            # from the exact fp32 value of the 16-bit W (which it reproduces bit
+            # for bit)
             for l in range(L):
                 self.dw[l].zero_()
-                T.tfd_apply_gradient_descent_matrix(self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
-                                                    var_bf16_t=self.weights_t[l], rounding=w.rounding)
+                if self.masters is not None:
+                    T.tfd_apply_gradient_descent_matrix(self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
+                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding)
+                else:
+                    wf = torch.empty(w.dims[l], w.dims[l + 1], dtype=torch.float32, device=dev)
+                    T.tfd_convert_bf16_to_f32(self.weights[l], wf)
+                    T.tfd_apply_gradient_descent_matrix(wf, 0.0, self.dw[l], var_bf16_t=self.weights_t[l])
 
         # pristine copies of the Variables, to restart from the same state
         self._saved = [t.clone() for t in self.variables()]

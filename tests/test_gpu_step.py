@@ -374,3 +374,15 @@ def _check_full_size(name):
 def test_full_size_step(name):
     flips = _check_full_size(name)
     print(f"{name}: {flips} rows with in-band Relu mask differences")
+
+
+@pytest.mark.parametrize("batch,dims", [(256, (512, 1024)), (130, (100, 1030))])
+def test_constant_weights_get_an_exact_transposed_copy(batch, dims):
+    """A 16-bit weight that is never updated (the tall layer) is also kept
+    transposed for the forward MatMul: the copy is W^T bit for bit."""
+    w = workloads.workload("tall512x32768-bf16").scaled(batch=batch, dims=dims)
+    s = DenseStep(w, workloads.generate(w, seed=9))
+    torch.cuda.synchronize()
+    assert s.forward_layout == "NT"
+    for W, Wt in zip(s.weights, s.weights_t):
+        assert torch.equal(Wt.view(torch.int16), W.t().contiguous().view(torch.int16))
