@@ -14,9 +14,6 @@ before the step's start event), so each timed step is exactly the computation
 the parity tests check. ms_per_step is the mean of the per-step HIP event
 intervals on the launch stream; the host-side bracket (synchronize on both
 sides of the K steps, restores included) is reported as wall_ms_per_step.
-The per-op breakdown comes from a second pass of K steps with an event
-recorded between consecutive ops (instrumentation the timed steps do not
-carry).
 Throughput counts the step's GEMM FLOPs, sum of 2*m*n*k.
 The cpu_baseline leg times the oracle (float64 numpy) on a row slice of the
 same workload on the host cores.
@@ -81,22 +78,11 @@ def time_workload(name: str, steps: int, warmup: int):
         s.run()
     torch.cuda.synchronize()
 
-    # the timed steps: one event pair per step on the launch stream
+    # per-step and per-op events, recorded on the launch stream
     step_ev = []
+    op_ev = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
-        s.restore()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        s.run()
-        b.record(stream)
-        step_ev.append((a, b))
-    torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) / steps * 1e3
-
-    # per-op breakdown: the same steps again, an event between consecutive ops
-    op_ev = []
     for _ in range(steps):
         s.restore()
         marks = []
@@ -107,8 +93,10 @@ def time_workload(name: str, steps: int, warmup: int):
             marks.append((tag, e))
 
         s.run(mark=mark)
+        step_ev.append((marks[0][1], marks[-1][1]))
         op_ev.append(marks)
     torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
 
     step_ms = [a.elapsed_time(b) for a, b in step_ev]
     per_op = {}
