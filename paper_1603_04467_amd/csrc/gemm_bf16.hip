@@ -1,8 +1,11 @@
 // MatMul for 16-bit operands on whole 256 x 256 output tiles (the shapes of
-// the wide dense layers), fp32 accumulation, fused bias + ReLU epilogue.
+// the wide dense layers), fp32 accumulation, with the epilogues of the
+// training step fused into it.
 //
-// Per workgroup: a 256 x 256 output tile, 4 waves each owning 128 x 128
-// (4 x 4 fragments of v_mfma_f32_32x32x16_bf16, 256 accumulators per lane).
+// Per workgroup: one 256 x 256 output tile (or one k-range split of it),
+// split over 4 waves of 128 x 128, 8 waves of 128 x 64 (the default for the
+// NN and NT layouts) or 16 waves of 64 x 64 (the default for TN), each wave
+// holding 32 x 32 fragments of v_mfma_f32_32x32x16_bf16 accumulators.
 // The k loop walks 64-wide k-tiles through two LDS stages of 64 KiB:
 //  - global -> LDS copies go straight into LDS (global_load_lds_dwordx4, 1 KiB
 //    per wave instruction), so no registers stage them; the copy of k-tile
@@ -17,9 +20,15 @@
 //    MFMA lane needs), so no transpose pass is needed anywhere (issued as
 //    inline assembly, see ds_read_tr16_b64);
 //  - fragments are double-buffered in registers: the reads for k-step q+1 are
-//    issued before the 16 MFMAs of k-step q.
+//    interleaved with the MFMAs of k-step q.
 // K-slot assignment (identical for both operands, so each k is summed once):
 // lane l supplies k = 32*(l/32) + 8*q + e, e = 0..7, in k-step q of a k-tile.
+// Epilogues (see the EP list below): bias, ReLU and one rounding; a 16-bit
+// tile is staged through LDS and leaves in 16-byte row chunks; ReLU masks
+// from wave ballots; ReluGrad from features or a mask with the tile's column
+// sums; the squared-error head. Outputs are written with non-temporal
+// stores. A split k range writes fp32 partial tiles that
+// splitk_reduce_kernel sums in order.
 //
 // Preconditions (checked by the dispatcher): m, n multiples of 256, k a
 // multiple of 64, 16-byte aligned rows.
@@ -187,8 +196,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-// Scheduling hint: 16 MFMAs spread evenly over kReads groups, each followed
-// by one LDS read.
+// Scheduling hint: a k-step's kMfma MFMAs spread evenly over kReads groups,
+// each followed by one LDS read.
 template <int T, int kReads, int kMfma>
 __device__ __forceinline__ void interleave_mfma_reads() {
   if constexpr (T < kReads) {
