@@ -247,12 +247,18 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
     __syncthreads();
   }
 
+  // The other stage is free from the barrier that opens k-tile t (every
+  // wave has finished reading it), so k-tile t+1 is fetched after the
+  // first k-step's fragment reads and written to LDS after the second
+  // k-step's MFMAs: both hide behind the matrix-core work of the current
+  // k-tile, and only the barrier and the first fragment reads remain
+  // between k-tiles. (Writing after the first k-step waits on loads still
+  // in flight; moving the barrier ahead of the last k-step's MFMAs to
+  // prefetch the next k-tile's first fragments spills registers in the
+  // loop. Both measured slower.)
+  constexpr int kStoreAfter = 1;
   for (int kt = 0; kt < kt_count; ++kt) {
     const bool more = kt + 1 < kt_count;
-    if (more) {
-      la.load(A, p.lda, m0, p.m, (kt + 1) * BK, p.k, tid);
-      lb.load(B, p.ldb, n0, p.n, (kt + 1) * BK, p.k, tid);
-    }
     const char* sa = smem + (kt & 1) * kStageBytes;
     const char* sb = sa + BM * 128;
 #pragma unroll
@@ -265,15 +271,19 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         fb[j] = *reinterpret_cast<const u32x4*>(sb + lds_off(wave_n * WTN + j * 32 + l32, chunk));
+      if (q == 0 && more) {
+        la.load(A, p.lda, m0, p.m, (kt + 1) * BK, p.k, tid);
+        lb.load(B, p.ldb, n0, p.n, (kt + 1) * BK, p.k, tid);
+      }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) mfma_chunk<T>(acc[i][j], fa[i], fb[j]);
-    }
-    if (more) {
-      char* st = smem + ((kt + 1) & 1) * kStageBytes;
-      la.store(st, tid);
-      lb.store(st + BM * 128, tid);
+      if (q == kStoreAfter && more) {
+        char* st = smem + ((kt + 1) & 1) * kStageBytes;
+        la.store(st, tid);
+        lb.store(st + BM * 128, tid);
+      }
     }
     __syncthreads();
   }
