@@ -17,7 +17,9 @@
 // both of TN) is loaded as V x V blocks (V = elements per 16 bytes) and
 // transposed in registers on the way to LDS. LDS is double-buffered: the
 // global loads of k-tile t+1 are in flight while the matrix cores consume
-// k-tile t, with one barrier per k-tile.
+// k-tile t, with one barrier per k-tile. fp32 problems of whole 256 x 256
+// tiles take gemm_f32_256 instead, whose copies go straight from global
+// memory into LDS and whose m/n-contiguous operands stay m/n-major there.
 //
 // K-slot assignment: within a k-tile, lanes 0-31 supply k in [0, BK/2) and
 // lanes 32-63 k in [BK/2, BK), eight (bf16) or one (fp32) per instruction,
@@ -202,6 +204,33 @@ __device__ __forceinline__ void mfma_chunk<bf16>(f32x16& acc, const u32x4& a, co
                                                 __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
 }
 
+// Epilogue: bias, Relu, one rounding to OutT, for a wave's FM x FN
+// fragments whose first output row / column are row0 / col0.
+template <typename OutT, int FM, int FN>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const f32x16 (&acc)[FM][FN], int row0, int col0,
+                                           int half, int l32) {
+  OutT* C = static_cast<OutT*>(p.c);
+  const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int col = col0 + j * 32 + l32;
+    const bool col_ok = col < p.n;
+    const float bv = ((p.epi & kEpiOpMask) != 0 && col_ok) ? p.bias[col] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (col_ok && row < p.m) {
+          float v = acc[i][j][r] + bv;
+          if ((p.epi & kEpiOpMask) == 2) v = relu_f32(v);
+          store_from_f32(C + (int64_t)row * p.ldc + col, v, trunc16);
+        }
+      }
+    }
+  }
+}
+
 template <typename T, typename OutT, bool TA, bool TB, int BM, int BN, int WM, int WN, bool ALIGNED>
 __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
   constexpr int NT = WM * WN * kWave;
@@ -288,27 +317,140 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
     __syncthreads();
   }
 
-  // Epilogue: bias, Relu, one rounding to OutT.
-  OutT* C = static_cast<OutT*>(p.c);
-  const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
+  store_tile<OutT, FM, FN>(p, acc, m0 + wave_m * WTM, n0 + wave_n * WTN, half, l32);
+}
+
+
+// Whole 256 x 256 fp32 tiles (m, n multiples of 256, k a multiple of 32,
+// 16-byte aligned rows): the same LDS stages, fragments and MFMAs as above,
+// with the copies going straight from global memory into LDS
+// (global_load_lds_dwordx4: 64 lanes x 16 bytes land contiguously in 1 KiB
+// of LDS), so that no registers stage them and no transpose pass or LDS
+// write instruction is needed. 8 waves of 128 x 64.
+//  - k-contiguous operand: the 128-byte-row layout above; in a 1 KiB block
+//    (8 rows) lane i fills slot i % 8 of row i / 8, i.e. it fetches the chunk
+//    that the row's swizzle puts in that slot.
+//  - m/n-contiguous operand: k-rows of 256 values (1 KiB), value mn of k-row
+//    kr at kr * 1024 + 16 * ((mn / 4) ^ mn_swz(kr)) + 4 * (mn % 4). A lane of
+//    a fragment read takes four consecutive k of one column (four ds_read_b32
+//    1 KiB apart, merged by the compiler into ds_read2st64_b32); mn_swz moves
+//    the k-rows 16..31, read by lanes 32..63 at the same time as lanes 0..31
+//    read rows 0..15, to the other 128 bytes of the banks.
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ int mn_swz(int krow) { return ((krow >> 4) & 1) << 3; }
+
+template <bool KC>
+__device__ __forceinline__ void copy_tile_f32(const float* X, int64_t ld, int mn0, int k0, char* lds, int wave,
+                                              int lane) {
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int col = n0 + wave_n * WTN + j * 32 + l32;
-    const bool col_ok = col < p.n;
-    const float bv = ((p.epi & kEpiOpMask) != 0 && col_ok) ? p.bias[col] : 0.0f;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wave_m * WTM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        if (col_ok && row < p.m) {
-          float v = acc[i][j][r] + bv;
-          if ((p.epi & kEpiOpMask) == 2) v = relu_f32(v);
-          store_from_f32(C + (int64_t)row * p.ldc + col, v, trunc16);
-        }
-      }
+  for (int j = 0; j < 4; ++j) {  // 32 blocks of 1 KiB per operand, 4 per wave
+    const int blk = wave * 4 + j;
+    const float* g;
+    if (KC) {
+      const int r = blk * 8 + (lane >> 3);
+      g = X + (int64_t)(mn0 + r) * ld + k0 + (((lane & 7) ^ swz(r)) << 2);
+    } else {
+      g = X + (int64_t)(k0 + blk) * ld + mn0 + ((lane ^ mn_swz(blk)) << 2);
     }
+    __builtin_amdgcn_global_load_lds(g, (lds_void*)(lds + blk * 1024), 16, 0, 0);
   }
+}
+
+// Four consecutive k (k0 .. k0+3, one group of 16 k-rows) of column mn of an
+// m/n-major operand tile.
+__device__ __forceinline__ u32x4 read_mn_f32(const char* tile, int mn, int k0) {
+  const char* q = tile + k0 * 1024 + (((mn >> 2) ^ mn_swz(k0)) << 4) + ((mn & 3) << 2);
+  u32x4 r;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) r[s] = *reinterpret_cast<const uint32_t*>(q + s * 1024);
+  return r;
+}
+
+template <bool TA, bool TB>
+__global__ __launch_bounds__(512) void gemm_f32_256(GemmParams p) {
+  constexpr int WN = 4, WTM = 128, WTN = 64, FM = WTM / 32, FN = WTN / 32;
+  constexpr bool A_KC = !TA, B_KC = TB;
+  constexpr int kOperandBytes = 256 * 128, kStageBytes = 2 * kOperandBytes;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kStageBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wave_m = wave / WN, wave_n = wave % WN;
+  const int half = lane >> 5, l32 = lane & 31;
+
+  int tm, tn;
+  tile_of_block(blockIdx.x, p.tiles_m, p.tiles_n, tm, tn);
+  const int m0 = tm * 256, n0 = tn * 256;
+  const float* A = static_cast<const float*>(p.a);
+  const float* B = static_cast<const float*>(p.b);
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int kt_count = p.k / 32;
+  copy_tile_f32<A_KC>(A, p.lda, m0, 0, smem, wave, lane);
+  copy_tile_f32<B_KC>(B, p.ldb, n0, 0, smem + kOperandBytes, wave, lane);
+  __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
+  __syncthreads();
+
+  for (int kt = 0; kt < kt_count; ++kt) {
+    const char* sa = smem + (kt & 1) * kStageBytes;
+    const char* sb = sa + kOperandBytes;
+    if (kt + 1 < kt_count) {
+      char* nx = smem + ((kt + 1) & 1) * kStageBytes;
+      copy_tile_f32<A_KC>(A, p.lda, m0, (kt + 1) * 32, nx, wave, lane);
+      copy_tile_f32<B_KC>(B, p.ldb, n0, (kt + 1) * 32, nx + kOperandBytes, wave, lane);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int chunk = half * 4 + q;  // k = 4 * chunk + s in MFMA sub-step s
+      u32x4 fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int r = wave_m * WTM + i * 32 + l32;
+        fa[i] = A_KC ? *reinterpret_cast<const u32x4*>(sa + lds_off(r, chunk)) : read_mn_f32(sa, r, 4 * chunk);
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int c = wave_n * WTN + j * 32 + l32;
+        fb[j] = B_KC ? *reinterpret_cast<const u32x4*>(sb + lds_off(c, chunk)) : read_mn_f32(sb, c, 4 * chunk);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) mfma_chunk<float>(acc[i][j], fa[i], fb[j]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of k-tile t+1 have landed
+    __syncthreads();
+  }
+
+  store_tile<float, FM, FN>(p, acc, m0 + wave_m * WTM, n0 + wave_n * WTN, half, l32);
+}
+
+template <bool TA, bool TB>
+hipError_t launch_f32_256(const GemmDesc& d, hipStream_t s) {
+  GemmParams p;
+  p.a = d.a;
+  p.b = d.b;
+  p.c = d.c;
+  p.bias = d.bias;
+  p.lda = d.lda;
+  p.ldb = d.ldb;
+  p.ldc = d.ldc;
+  p.m = (int)d.m;
+  p.n = (int)d.n;
+  p.k = (int)d.k;
+  p.epi = d.epi;
+  p.tiles_m = (int)(d.m / 256);
+  p.tiles_n = (int)(d.n / 256);
+  hipLaunchKernelGGL((gemm_f32_256<TA, TB>), dim3(p.tiles_m * p.tiles_n), dim3(512), 0, s, p);
+  return hipGetLastError();
 }
 
 template <typename T, typename OutT, bool TA, bool TB, int BM, int BN, int WM, int WN, bool ALIGNED>
@@ -339,8 +481,10 @@ hipError_t launch_cfg(const GemmDesc& d, hipStream_t s) {
 // 5 = 256x256 (8 waves of 128x64), 6 = 256x256 (16 waves of 64x64),
 // 7 = 128x128 (8 waves of 64x32), 8 = the small-problem kernel of
 // gemm_small.hip (the default for fp32 problems with fewer than 128 tiles of
-// 128 x 128). Non-zero values come from the tuning-only environment variable
-// TFD_GEMM_TILE.
+// 128 x 128), 9 = the whole-tile direct-to-LDS kernel gemm_f32_256 (8 waves
+// of 128x64; the default for fp32 problems of whole 256 x 256 tiles and at
+// least 128 of them, else 5 takes its place). Non-zero values come from the
+// tuning-only environment variable TFD_GEMM_TILE.
 template <typename T, typename OutT, bool TA, bool TB>
 hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t s) {
   if (!aligned) return launch_cfg<T, OutT, TA, TB, 64, 64, 2, 2, false>(d, s);
@@ -348,10 +492,13 @@ hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t 
     const int64_t tiles256 = ((d.m + 255) / 256) * ((d.n + 255) / 256);
     const int64_t tiles128 = ((d.m + 127) / 128) * ((d.n + 127) / 128);
     // fp32: 256x256 with 8 waves (2 per SIMD) measured fastest inside the step
-    tile = tiles256 >= 128 ? (sizeof(T) == 4 ? 5 : 1) : (tiles128 >= 128 ? 3 : 4);
+    tile = tiles256 >= 128 ? (sizeof(T) == 4 ? 9 : 1) : (tiles128 >= 128 ? 3 : 4);
   }
   if constexpr (sizeof(T) == 4) {  // fp32-only shapes
+    const bool whole = d.m % 256 == 0 && d.n % 256 == 0 && d.k % 32 == 0 && d.k > 0;
+    if (tile == 9 && whole) return launch_f32_256<TA, TB>(d, s);
     switch (tile) {
+      case 9:
       case 5: return launch_cfg<T, OutT, TA, TB, 256, 256, 2, 4, true>(d, s);
       case 6: return launch_cfg<T, OutT, TA, TB, 256, 256, 4, 4, true>(d, s);
       case 7: return launch_cfg<T, OutT, TA, TB, 128, 128, 2, 4, true>(d, s);

@@ -103,7 +103,7 @@ def test_matmul_parity(m, n, k, layout, din, dout):
         assert bad == 0, f"{bad} Relu mask decisions differ outside the rounding band"
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6, 7, 8, 9])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
 @pytest.mark.parametrize("din,dout", TYPES)
 def test_matmul_every_tile_config(tile, layout, din, dout):
@@ -113,6 +113,21 @@ def test_matmul_every_tile_config(tile, layout, din, dout):
 
 
 WHOLE_TILES = [(256, 256, 64), (512, 768, 192), (768, 512, 1024), (1024, 256, 4096)]
+
+
+@pytest.mark.parametrize("epi", ["none", "bias", "bias_relu"])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("m,n,k", [(256, 256, 32), *WHOLE_TILES])
+def test_matmul_f32_whole_tiles(m, n, k, layout, epi):
+    """fp32 operands on whole 256 x 256 tiles: the direct-to-LDS kernel
+    (configuration 9, the default from 128 such tiles up), one k-tile and
+    many, against the oracle."""
+    got, want, pre, D = _run_gemm(m, n, k, layout, "f32", "f32", epi, seed=k + 1, tile=9)
+    assert_close(got, want, D, TAU["f32"], f"{layout} f32 {m}x{n}x{k} {epi}")
+    if epi == "bias_relu":
+        assert not np.any(np.signbit(got)), "Relu output with a sign bit"
+        bad, _ = mask_mismatch(got, pre, TAU["f32"] * D)
+        assert bad == 0
 
 
 @pytest.mark.parametrize("epi", ["none", "bias", "bias_relu"])
@@ -187,6 +202,14 @@ def test_matmul_leading_dimensions(layout, ld_extra):
     assert_close(got, want, D, TAU["f32"], f"ld+{ld_extra} {layout}")
     got, want, _, D = _run_gemm(130, 72, 88, layout, "bf16", "bf16", "bias", ld_extra=ld_extra)
     assert_close(got, want, D, TAU["bf16"], f"ld+{ld_extra} {layout} bf16")
+
+
+@pytest.mark.parametrize("ld_extra", [4, 36])
+@pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
+def test_matmul_f32_whole_tiles_leading_dimensions(layout, ld_extra):
+    """Strided operands and output in the fp32 whole-tile kernel."""
+    got, want, _, D = _run_gemm(512, 256, 96, layout, "f32", "f32", "bias", ld_extra=ld_extra, tile=9)
+    assert_close(got, want, D, TAU["f32"], f"ld+{ld_extra} {layout} whole tiles")
 
 
 def test_matmul_k_zero_gives_relu_of_bias():
