@@ -322,8 +322,8 @@ __global__ __launch_bounds__(WM * WN * kWave) void gemm_kernel(GemmParams p) {
 
 
 // Whole 256 x 256 fp32 tiles (m, n multiples of 256, k a multiple of 32,
-// 16-byte aligned rows): the same LDS stages, fragments and MFMAs as above,
-// with the copies going straight from global memory into LDS
+// 16-byte aligned rows): the same two LDS stages, k-slot assignment and
+// MFMAs as above, with the copies going straight from global memory into LDS
 // (global_load_lds_dwordx4: 64 lanes x 16 bytes land contiguously in 1 KiB
 // of LDS), so that no registers stage them and no transpose pass or LDS
 // write instruction is needed. 8 waves of 128 x 64.
