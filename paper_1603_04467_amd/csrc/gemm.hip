@@ -399,35 +399,61 @@ __global__ __launch_bounds__(512) void gemm_f32_256(GemmParams p) {
   __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
   __syncthreads();
 
+  // Fragments of k-step q (k = 4 * chunk + s in MFMA sub-step s).
+  auto read_frags = [&](const char* st, int q, u32x4 (&a_)[FM], u32x4 (&b_)[FN]) {
+    const char* sb = st + kOperandBytes;
+    const int chunk = half * 4 + q;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r = wave_m * WTM + i * 32 + l32;
+      a_[i] = A_KC ? *reinterpret_cast<const u32x4*>(st + lds_off(r, chunk)) : read_mn_f32(st, r, 4 * chunk);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int c = wave_n * WTN + j * 32 + l32;
+      b_[j] = B_KC ? *reinterpret_cast<const u32x4*>(sb + lds_off(c, chunk)) : read_mn_f32(sb, c, 4 * chunk);
+    }
+  };
+  // NN and NT pass the barrier that publishes k-tile t+1 before the last
+  // k-step's MFMAs of k-tile t and read k-tile t+1's first fragments behind
+  // them (measured 0.3 % and 1.6 % faster; TN, whose operands are both
+  // read as dword pairs, 0.5 % slower).
+  constexpr bool kEarlyBarrier = !TA;
+  u32x4 fa[FM], fb[FN], na[FM], nb[FN];
+  if constexpr (kEarlyBarrier) read_frags(smem, 0, na, nb);
+
   for (int kt = 0; kt < kt_count; ++kt) {
     const char* sa = smem + (kt & 1) * kStageBytes;
-    const char* sb = sa + kOperandBytes;
-    if (kt + 1 < kt_count) {
-      char* nx = smem + ((kt + 1) & 1) * kStageBytes;
+    char* nx = smem + ((kt + 1) & 1) * kStageBytes;
+    const bool more = kt + 1 < kt_count;
+    if (more) {
       copy_tile_f32<A_KC>(A, p.lda, m0, (kt + 1) * 32, nx, wave, lane);
       copy_tile_f32<B_KC>(B, p.ldb, n0, (kt + 1) * 32, nx + kOperandBytes, wave, lane);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int chunk = half * 4 + q;  // k = 4 * chunk + s in MFMA sub-step s
-      u32x4 fa[FM], fb[FN];
+      if (kEarlyBarrier && q == 0) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int r = wave_m * WTM + i * 32 + l32;
-        fa[i] = A_KC ? *reinterpret_cast<const u32x4*>(sa + lds_off(r, chunk)) : read_mn_f32(sa, r, 4 * chunk);
+        for (int i = 0; i < FM; ++i) fa[i] = na[i];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[j] = nb[j];
+      } else {
+        read_frags(sa, q, fa, fb);
       }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int c = wave_n * WTN + j * 32 + l32;
-        fb[j] = B_KC ? *reinterpret_cast<const u32x4*>(sb + lds_off(c, chunk)) : read_mn_f32(sb, c, 4 * chunk);
+      if (kEarlyBarrier && q == 3) {
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of k-tile t+1 have landed
+        __syncthreads();
+        if (more) read_frags(nx, 0, na, nb);
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) mfma_chunk<float>(acc[i][j], fa[i], fb[j]);
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of k-tile t+1 have landed
-    __syncthreads();
+    if constexpr (!kEarlyBarrier) {
+      __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of k-tile t+1 have landed
+      __syncthreads();
+    }
   }
 
   store_tile<float, FM, FN>(p, acc, m0 + wave_m * WTM, n0 + wave_n * WTN, half, l32);
