@@ -634,6 +634,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 }  // namespace
 
+#ifdef TFD_GEMM_BF16_TN_UNIT
+// The TN layout (both operands m/n-contiguous, transposing reads), built from
+// this file in a translation unit of its own (gemm_bf16_tn.hip) so that it
+// can take its own machine-scheduler setting.
+hipError_t launch_gemm_bf16_256_tn(const GemmDesc& d, hipStream_t s) {
+  return launch_waves<false, false>(d, waves_for("TN", 16), s);
+}
+#else
 int gemm_bf16_256_splits(const GemmDesc& d, int cus) {
   // split the k range when the output has fewer whole tiles than compute
   // units, keeping at least 8 k-tiles per split
@@ -677,7 +685,8 @@ hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // from more waves to hide LDS latency.
   if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for("NN", 8), s);
   if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for("NT", 8), s);
-  return launch_waves<false, false>(d, waves_for("TN", 16), s);
+  return launch_gemm_bf16_256_tn(d, s);
 }
+#endif
 
 }  // namespace tfd

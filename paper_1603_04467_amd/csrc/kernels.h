@@ -57,6 +57,8 @@ int gemm_tile_override();
 // 16-bit operands, whole 256 x 256 tiles, k a multiple of 64 (gemm_bf16.hip).
 bool gemm_bf16_256_ok(const GemmDesc& d);
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s);
+// Its TN layout, compiled in gemm_bf16_tn.hip.
+hipError_t launch_gemm_bf16_256_tn(const GemmDesc& d, hipStream_t s);
 // Number of k splits worth using for a whole-tile 16-bit problem on `cus`
 // compute units (1: none).
 int gemm_bf16_256_splits(const GemmDesc& d, int cus);
