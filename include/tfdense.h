@@ -20,7 +20,8 @@
  *    gradients and Variables are always fp32.
  *  - Pointers are device pointers unless stated otherwise. The caller owns
  *    every buffer; the library allocates no device memory, keeps no state
- *    between calls and never synchronises. Scratch memory is passed in as a
+ *    between calls (besides the tuning knobs of tfd_set_tuning) and never
+ *    synchronises. Scratch memory is passed in as a
  *    "workspace" sized by the matching *_workspace_size call.
  *  - Every call enqueues its kernels on `stream` (a hipStream_t passed as
  *    void*; NULL is the null stream) and returns. Stream order is the only
@@ -47,7 +48,7 @@
 extern "C" {
 #endif
 
-#define TFD_ABI_VERSION 4
+#define TFD_ABI_VERSION 5
 
 #if defined(__GNUC__)
 #define TFD_API __attribute__((visibility("default")))
@@ -88,6 +89,25 @@ TFD_API int tfd_abi_version(void);
 TFD_API const char* tfd_status_string(tfd_status status);
 /* Message of the last failed call on this host thread ("" if none). */
 TFD_API const char* tfd_last_error(void);
+
+/*
+ * Tuning and testing only (not part of the paper's ops): force a kernel
+ * configuration that the library would otherwise choose itself, so that
+ * every configuration can be measured and parity-tested. The setting is
+ * process-wide and lasts until it is set again; 0 restores the library's
+ * own choice. The default dispatch reads neither these knobs' defaults nor
+ * the environment from anywhere else. Knobs:
+ *   "gemm_tile"      1..9: the tile configuration of the general MatMul
+ *                    kernels (which also disables the 16-bit whole-tile
+ *                    kernel and the k split);
+ *   "bf16_waves_nn", "bf16_waves_nt", "bf16_waves_tn"
+ *                    4, 8 or 16: waves per workgroup of the 16-bit
+ *                    whole-tile MatMul for that layout;
+ *   "small_waves"    4, 8 or 16: waves per tile of the small fp32 MatMul.
+ * Returns TFD_EINVAL for an unknown knob or a value out of range. Calls that
+ * are in flight on other host threads may see either setting.
+ */
+TFD_API tfd_status tfd_set_tuning(const char* knob, int value);
 
 /*
  * MatMul (section 2, Table 1) with the op's transpose attributes, fused with

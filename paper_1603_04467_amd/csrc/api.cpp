@@ -5,6 +5,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "../../include/tfdense.h"
 #include "kernels.h"
 
@@ -61,6 +63,48 @@ const char* tfd_status_string(tfd_status s) {
 }
 
 const char* tfd_last_error(void) { return g_err; }
+
+}  // extern "C"
+
+namespace {
+
+std::atomic<int> g_tune[tfd::kTuneCount];
+
+struct KnobSpec {
+  const char* name;
+  tfd::TuneKnob knob;
+  int lo, hi;      // accepted range besides 0
+  bool waves;      // only 4, 8 or 16
+};
+
+constexpr KnobSpec kKnobs[] = {
+    {"gemm_tile", tfd::kTuneGemmTile, 1, 9, false},
+    {"bf16_waves_nn", tfd::kTuneBf16WavesNN, 4, 16, true},
+    {"bf16_waves_nt", tfd::kTuneBf16WavesNT, 4, 16, true},
+    {"bf16_waves_tn", tfd::kTuneBf16WavesTN, 4, 16, true},
+    {"small_waves", tfd::kTuneSmallWaves, 4, 16, true},
+};
+
+}  // namespace
+
+namespace tfd {
+int tuning(TuneKnob knob) { return g_tune[knob].load(std::memory_order_relaxed); }
+}  // namespace tfd
+
+extern "C" {
+
+tfd_status tfd_set_tuning(const char* knob, int value) {
+  if (!knob) return fail(TFD_EINVAL, "tfd_set_tuning: null knob name");
+  for (const KnobSpec& k : kKnobs) {
+    if (strcmp(k.name, knob) != 0) continue;
+    const bool ok = value == 0 || (k.waves ? (value == 4 || value == 8 || value == 16)
+                                           : (value >= k.lo && value <= k.hi));
+    if (!ok) return fail(TFD_EINVAL, "tfd_set_tuning: value %d out of range for %s", value, knob);
+    g_tune[k.knob].store(value, std::memory_order_relaxed);
+    return TFD_OK;
+  }
+  return fail(TFD_EINVAL, "tfd_set_tuning: unknown knob %s", knob);
+}
 
 }  // extern "C"
 

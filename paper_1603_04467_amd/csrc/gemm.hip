@@ -510,7 +510,7 @@ hipError_t launch_cfg(const GemmDesc& d, hipStream_t s) {
 // 128 x 128), 9 = the whole-tile direct-to-LDS kernel gemm_f32_256 (8 waves
 // of 128x64; the default for fp32 problems of whole 256 x 256 tiles and at
 // least 128 of them, else 5 takes its place). Non-zero values come from the
-// tuning-only environment variable TFD_GEMM_TILE.
+// "gemm_tile" tuning knob (tfd_set_tuning).
 template <typename T, typename OutT, bool TA, bool TB>
 hipError_t launch_layout(const GemmDesc& d, bool aligned, int tile, hipStream_t s) {
   if (!aligned) return launch_cfg<T, OutT, TA, TB, 64, 64, 2, 2, false>(d, s);
@@ -547,11 +547,6 @@ hipError_t launch_types(const GemmDesc& d, bool aligned, int tile, hipStream_t s
 }
 
 }  // namespace
-
-int gemm_tile_override() {
-  const char* e = getenv("TFD_GEMM_TILE");
-  return e ? atoi(e) : 0;
-}
 
 // Vector (16-byte) loads are legal when every row start of both operands is
 // 16-byte aligned and each operand's contiguous extent is whole chunks.

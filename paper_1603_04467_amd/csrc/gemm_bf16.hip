@@ -33,9 +33,6 @@
 // Preconditions (checked by the dispatcher): m, n multiples of 256, k a
 // multiple of 64, 16-byte aligned rows.
 
-#include <stdlib.h>
-#include <string.h>
-
 #include <type_traits>
 
 #include "common.h"
@@ -589,14 +586,11 @@ hipError_t launch_waves(const GemmDesc& d, int waves, hipStream_t s) {
   return launch<A_KC, B_KC, 2, 4>(d, s);
 }
 
-// Tuning-only override "NN:8,NT:4,TN:16" (environment variable TFD_BF16_WAVES).
-int waves_for(const char* layout, int dflt) {
-  const char* e = getenv("TFD_BF16_WAVES");
-  if (!e) return dflt;
-  const char* f = strstr(e, layout);
-  if (!f) return dflt;
-  const int v = atoi(f + 3);
-  return (v == 4 || v == 8 || v == 16) ? v : dflt;
+// Waves per workgroup of a layout: the tuning knob when set (4, 8 or 16),
+// else the default.
+int waves_for(TuneKnob knob, int dflt) {
+  const int v = tuning(knob);
+  return v ? v : dflt;
 }
 
 }  // namespace
@@ -639,7 +633,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 // this file in a translation unit of its own (gemm_bf16_tn.hip) so that it
 // can take its own machine-scheduler setting.
 hipError_t launch_gemm_bf16_256_tn(const GemmDesc& d, hipStream_t s) {
-  return launch_waves<false, false>(d, waves_for("TN", 16), s);
+  return launch_waves<false, false>(d, waves_for(kTuneBf16WavesTN, 16), s);
 }
 #else
 int gemm_bf16_256_splits(const GemmDesc& d, int cus) {
@@ -683,8 +677,8 @@ hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // Defaults measured inside the training step: 8 waves (2 per SIMD) for
   // NN and NT, 16 waves for TN, whose two transposing-read operands gain most
   // from more waves to hide LDS latency.
-  if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for("NN", 8), s);
-  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for("NT", 8), s);
+  if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, 8), s);
+  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, 8), s);
   return launch_gemm_bf16_256_tn(d, s);
 }
 #endif

@@ -248,10 +248,7 @@ hipError_t launch_gemm_small_f32(const GemmDesc& d, hipStream_t s) {
   // 4 waves per tile: measured fastest for every MNIST-shaped problem, also
   // those with only a few tiles (8 or 16 waves per tile were slower)
   int waves = 4;
-  if (const char* e = getenv("TFD_SMALL_WAVES")) {  // tuning-only override: 4, 8 or 16
-    const int v = atoi(e);
-    if (v == 4 || v == 8 || v == 16) waves = v;
-  }
+  if (const int v = tuning(kTuneSmallWaves)) waves = v;  // tuning knob: 4, 8 or 16
   const int64_t per = (d.k + waves - 1) / waves;
   p.kper = (int)(((per + 7) / 8) * 8);
   if (p.kper == 0) p.kper = 8;

@@ -52,8 +52,11 @@ constexpr int kEpiTrunc16 = 16;
 
 bool gemm_vector_ok(const GemmDesc& d, int elem_bytes);
 hipError_t launch_gemm(const GemmDesc& d, hipStream_t s);
-// The TFD_GEMM_TILE tuning override (0 when unset).
-int gemm_tile_override();
+// Tuning knobs set through tfd_set_tuning (0: the library's own choice). The
+// default dispatch never reads the environment.
+enum TuneKnob { kTuneGemmTile = 0, kTuneBf16WavesNN, kTuneBf16WavesNT, kTuneBf16WavesTN, kTuneSmallWaves, kTuneCount };
+int tuning(TuneKnob knob);
+inline int gemm_tile_override() { return tuning(kTuneGemmTile); }
 // 16-bit operands, whole 256 x 256 tiles, k a multiple of 64 (gemm_bf16.hip).
 bool gemm_bf16_256_ok(const GemmDesc& d);
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s);

@@ -19,8 +19,7 @@ from typing import Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# TFD_LIBRARY points at another build of the same library (tuning variants).
-LIB_PATH = os.environ.get("TFD_LIBRARY") or os.path.join(_HERE, "libtfdense.so")
+LIB_PATH = os.path.join(_HERE, "libtfdense.so")
 
 TFD_OK, TFD_EINVAL, TFD_EUNSUPPORTED, TFD_EHIP = 0, 1, 2, 3
 TFD_F32, TFD_BF16 = 0, 1
@@ -38,6 +37,7 @@ EXPORTS = (
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
     "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
     "tfd_matmul_relu_mask_grad_bias_add_grad", "tfd_matmul_workspace_size", "tfd_matmul_with_workspace",
+    "tfd_set_tuning",
 )
 
 
@@ -50,15 +50,20 @@ class TfdError(RuntimeError):
 _lib = None
 
 
-def load() -> ctypes.CDLL:
+def load(path: Optional[str] = None) -> ctypes.CDLL:
     """Load libtfdense (torch is imported first so that the library binds to
-    the HIP runtime torch already uses)."""
+    the HIP runtime torch already uses). ``path`` loads another build of the
+    same library instead (an explicit choice of the caller, e.g. a tuning
+    variant); the first load fixes the library for the process."""
     global _lib
     if _lib is not None:
+        if path is not None and os.path.abspath(path) != _lib._name:
+            raise RuntimeError(f"libtfdense is already loaded from {_lib._name}")
         return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_1603_04467_amd.build`")
-    lib = ctypes.CDLL(LIB_PATH)
+    lib_path = os.path.abspath(path) if path is not None else LIB_PATH
+    if not os.path.exists(lib_path):
+        raise RuntimeError(f"{lib_path} is not built; run `python -m paper_1603_04467_amd.build`")
+    lib = ctypes.CDLL(lib_path)
     i64, vp, i32, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     sig = {
         "tfd_abi_version": ([], i32),
@@ -93,6 +98,7 @@ def load() -> ctypes.CDLL:
         "tfd_relu_mask_grad_bias_add_grad": ([vp, vp, vp, vp, i64, i64, i32, vp, sz, vp], i32),
         "tfd_matmul_relu_mask_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32,
                                                      vp, sz, vp], i32),
+        "tfd_set_tuning": ([ctypes.c_char_p, i32], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -143,6 +149,33 @@ def _flat(t: torch.Tensor, name: str):
 
 def tfd_abi_version() -> int:
     return load().tfd_abi_version()
+
+
+TUNING_KNOBS = ("gemm_tile", "bf16_waves_nn", "bf16_waves_nt", "bf16_waves_tn", "small_waves")
+
+
+def tfd_set_tuning(knob: str, value: int):
+    """Force a kernel configuration (tuning and tests only; 0 restores the
+    library's choice; see include/tfdense.h)."""
+    _check(load().tfd_set_tuning(knob.encode(), int(value)))
+
+
+class tuning:
+    """Context manager: ``with tuning(gemm_tile=9, bf16_waves_nt=4): ...``
+    sets knobs and restores the library's choice (0) on exit."""
+
+    def __init__(self, **knobs):
+        self.knobs = knobs
+
+    def __enter__(self):
+        for k, v in self.knobs.items():
+            tfd_set_tuning(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        for k in self.knobs:
+            tfd_set_tuning(k, 0)
+        return False
 
 
 def tfd_matmul_workspace_size(m, n, k, a_dtype, c_dtype, transpose_a=False, transpose_b=False) -> int:

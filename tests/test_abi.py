@@ -41,11 +41,23 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.tfd_abi_version() == 4
+    assert lib.tfd_abi_version() == 5
     assert lib.tfd_status_string(0) == b"ok"
     assert lib.tfd_status_string(1) == b"invalid argument"
     assert lib.tfd_status_string(2) == b"unsupported"
     assert lib.tfd_status_string(3) == b"HIP runtime error"
+
+
+def test_tuning_knobs(lib):
+    """The tuning entry point validates knob names and values (no GPU work)."""
+    for knob, bad in ((b"gemm_tile", 10), (b"gemm_tile", -1), (b"bf16_waves_nt", 6), (b"small_waves", 32),
+                      (b"no_such_knob", 4)):
+        assert lib.tfd_set_tuning(knob, bad) == 1
+    assert lib.tfd_set_tuning(None, 0) == 1
+    for knob, good in ((b"gemm_tile", 9), (b"bf16_waves_nn", 4), (b"bf16_waves_nt", 16), (b"bf16_waves_tn", 8),
+                       (b"small_waves", 8)):
+        assert lib.tfd_set_tuning(knob, good) == 0
+        assert lib.tfd_set_tuning(knob, 0) == 0
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first

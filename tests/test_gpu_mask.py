@@ -13,6 +13,7 @@ import torch
 import oracle
 from paper_1603_04467_amd import tfdense as T
 from paper_1603_04467_amd.workloads import to_bf16_bits
+from tests.parity import C_ACC, U32, assert_elementwise, product_bound, ulp  # noqa: F401
 from tests.parity import TAU, amax, assert_bits, assert_close, to_f64
 
 pytestmark = pytest.mark.gpu
@@ -55,9 +56,17 @@ def test_relu_mask_bit_exact(dt, rows, cols):
     assert np.array_equal(_words(m), oracle.relu_mask(f_h))
 
 
-def _set_waves(monkeypatch, waves):
-    if waves is not None:
-        monkeypatch.setenv("TFD_BF16_WAVES", f"NN:{waves},NT:{waves},TN:{waves}")
+@pytest.fixture
+def waves_knob():
+    """Sets the 16-bit whole-tile kernel's waves per workgroup for every
+    layout (tuning knob) and restores the library's choice afterwards."""
+    def set_(waves):
+        if waves is not None:
+            for lay in ("nn", "nt", "tn"):
+                T.tfd_set_tuning(f"bf16_waves_{lay}", waves)
+    yield set_
+    for lay in ("nn", "nt", "tn"):
+        T.tfd_set_tuning(f"bf16_waves_{lay}", 0)
 
 
 @pytest.mark.parametrize("m,n,k,layout,dt,rounding,waves", [
@@ -74,8 +83,8 @@ def _set_waves(monkeypatch, waves):
     (256, 10, 1024, "NN", "f32", "nearest", None),
     (0, 64, 32, "NT", "bf16", "nearest", None),
 ])
-def test_matmul_relu_mask(m, n, k, layout, dt, rounding, waves, monkeypatch):
-    _set_waves(monkeypatch, waves)
+def test_matmul_relu_mask(m, n, k, layout, dt, rounding, waves, waves_knob):
+    waves_knob(waves)
     rng = np.random.default_rng([m, n, k, len(layout), dt == "bf16", rounding == "truncate"])
     ta, tb = layout == "TN", layout == "NT"
     a_h, a = _host(rng, (k, m) if ta else (m, k), dt)
@@ -138,8 +147,8 @@ def test_relu_mask_grad_bias_add_grad(dt, rows, cols):
     (1024, 512, 256, "NT", "f32", "nearest", None),
     (0, 64, 32, "NT", "bf16", "nearest", None),         # no rows: bias_grad = 0
 ])
-def test_matmul_relu_mask_grad_bias_add_grad(m, n, k, layout, dt, rounding, waves, monkeypatch):
-    _set_waves(monkeypatch, waves)
+def test_matmul_relu_mask_grad_bias_add_grad(m, n, k, layout, dt, rounding, waves, waves_knob):
+    waves_knob(waves)
     rng = np.random.default_rng([m, n, k, len(layout), dt == "bf16", rounding == "truncate", 11])
     ta, tb = layout == "TN", layout == "NT"
     a_h, a = _host(rng, (k, m) if ta else (m, k), dt, zeros=0.0)
@@ -157,13 +166,27 @@ def test_matmul_relu_mask_grad_bias_add_grad(m, n, k, layout, dt, rounding, wave
     torch.cuda.synchronize()
     assert torch.equal(bp, bp2), "backprops differ from the features-based call"
     assert torch.equal(db, db2), "bias_grad differs from the features-based call"
+    # the plain MatMul on the same operands: the fused dY is the oracle's
+    # ReluGrad of its output from the mask, bit for bit (an exact select)
+    g = torch.full((m, n), float("nan"), dtype=tdt, device=DEV)
+    T.tfd_matmul(a, b, g, transpose_a=ta, transpose_b=tb, rounding=rounding)
+    torch.cuda.synchronize()
+    dy = to_f64(bp)
+    assert_bits(dy, oracle.relu_grad_from_mask(to_f64(g), oracle.relu_mask(f_h)), "fused dY = ReluGrad(plain output)")
     store = "bf16t" if rounding == "truncate" else dt
     want = oracle.relu_grad_from_mask(oracle.matmul(a_h, b_h, ta, tb, out=store), oracle.relu_mask(f_h))
     Dg = max(k, 1) * amax(a_h) * amax(b_h)
-    assert_close(to_f64(bp), want, Dg, TAU[dt], "fused dY")
-    dy = to_f64(bp)
+    assert_close(dy, want, Dg, TAU[dt], "fused dY")
     D = max(m, 1) * max(amax(dy), 1e-30)
     assert_close(to_f64(db), oracle.bias_add_grad(dy), D, TAU["f32"], "fused BiasAddGrad")
+    if m > 0:
+        keep = f_h > 0
+        A, B = (a_h.T if ta else a_h), (b_h.T if tb else b_h)
+        bound = product_bound(np.abs(A) @ np.abs(B), k, dy, store)
+        assert_elementwise(np.where(keep, dy, 0.0), np.where(keep, oracle.matmul(A, B, out="f64"), 0.0), bound,
+                           "fused dY per element")
+        cbound = C_ACC * m * U32 * np.abs(dy).sum(axis=0) + 0.5 * ulp(to_f64(db), "f32")
+        assert_elementwise(to_f64(db), oracle.bias_add_grad(dy, out="f64"), cbound, "fused db per column")
 
 
 @pytest.mark.parametrize("rounding", ["nearest", "truncate"])

@@ -6,8 +6,6 @@ configuration, ragged tails, unaligned rows (the per-element load path) and
 strided leading dimensions.
 """
 
-import os
-
 import numpy as np
 import pytest
 import torch
@@ -15,7 +13,8 @@ import torch
 import oracle
 from paper_1603_04467_amd import tfdense as T
 from paper_1603_04467_amd.workloads import to_bf16_bits
-from tests.parity import TAU, amax, assert_bits, assert_close, mask_mismatch, to_f64
+from tests.parity import (TAU, amax, assert_bits, assert_close, assert_elementwise, check_relu_decisions,
+                          mask_mismatch, product_bound, to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -55,6 +54,23 @@ def _strided(host, t, extra):
     return big[:, : t.shape[1]]
 
 
+def _check_elementwise(got, a_h, b_h, ta, tb, bias_h, epi, store, what):
+    """Per-element product bound on the operands the kernel read, and exact
+    ReLU decisions outside its band."""
+    A = a_h.T if ta else a_h
+    B = b_h.T if tb else b_h
+    K = A.shape[1]
+    y = oracle.matmul(A, B, out="f64", bias=None if epi == "none" else bias_h)
+    bound = product_bound(np.abs(A) @ np.abs(B), K, got, store,
+                          abs_bias=None if epi == "none" else np.abs(bias_h))
+    assert_elementwise(got, oracle.relu(y) if epi == "bias_relu" else y, bound, what)
+    if epi == "bias_relu":
+        check_relu_decisions(got, y, bound, what)
+
+
+_LAST = {}   # host operands of the latest _run_gemm call
+
+
 def _run_gemm(m, n, k, layout, din, dout, epi, seed=0, kind="normal", ld_extra=0, tile=None):
     rng = np.random.default_rng([seed, m, n, k])
     ta, tb = layout == "TN", layout == "NT"
@@ -67,20 +83,12 @@ def _run_gemm(m, n, k, layout, din, dout, epi, seed=0, kind="normal", ld_extra=0
         bias = torch.from_numpy(bias_h).to(DEV)
         bias_h = bias_h.astype(np.float64)
     c = _empty((m, n), dout, ld=n + ld_extra if ld_extra else None)
-    old = os.environ.get("TFD_GEMM_TILE")
-    if tile is not None:
-        os.environ["TFD_GEMM_TILE"] = str(tile)
-    try:
+    with T.tuning(gemm_tile=tile or 0):
         T.tfd_matmul(a, b, c, transpose_a=ta, transpose_b=tb, bias=bias, epilogue=epi)
         torch.cuda.synchronize()
-    finally:
-        if tile is not None:
-            if old is None:
-                del os.environ["TFD_GEMM_TILE"]
-            else:
-                os.environ["TFD_GEMM_TILE"] = old
     want = oracle.matmul(a_h, b_h, ta, tb, out=dout, bias=bias_h, relu=epi == "bias_relu")
     pre = oracle.matmul(a_h, b_h, ta, tb, out="f64", bias=bias_h)
+    _LAST.update(a=a_h, b=b_h, bias=bias_h)
     D = k * amax(a_h) * amax(b_h) + (amax(bias_h) if bias_h is not None else 0.0)
     return to_f64(c), want, pre, D
 
@@ -97,6 +105,9 @@ def test_matmul_parity(m, n, k, layout, din, dout):
     epi = "bias_relu" if layout == "NN" else "none"
     got, want, pre, D = _run_gemm(m, n, k, layout, din, dout, epi)
     assert_close(got, want, D, TAU[din], f"{layout} {din}->{dout} {m}x{n}x{k}")
+    a_h, b_h, bias_h = _LAST["a"], _LAST["b"], _LAST["bias"]
+    _check_elementwise(got, a_h, b_h, layout == "TN", layout == "NT", bias_h, epi, dout,
+                       f"{layout} {din}->{dout} {m}x{n}x{k} per element")
     if epi == "bias_relu":
         assert not np.any(np.signbit(got)), "Relu output with a sign bit"
         bad, _ = mask_mismatch(got, pre, TAU[din] * D)
@@ -124,6 +135,8 @@ def test_matmul_f32_whole_tiles(m, n, k, layout, epi):
     many, against the oracle."""
     got, want, pre, D = _run_gemm(m, n, k, layout, "f32", "f32", epi, seed=k + 1, tile=9)
     assert_close(got, want, D, TAU["f32"], f"{layout} f32 {m}x{n}x{k} {epi}")
+    _check_elementwise(got, _LAST["a"], _LAST["b"], layout == "TN", layout == "NT", _LAST["bias"], epi, "f32",
+                       f"{layout} f32 {m}x{n}x{k} {epi} per element")
     if epi == "bias_relu":
         assert not np.any(np.signbit(got)), "Relu output with a sign bit"
         bad, _ = mask_mismatch(got, pre, TAU["f32"] * D)
@@ -138,6 +151,8 @@ def test_matmul_bf16_whole_tiles(m, n, k, layout, dout, epi):
     """16-bit operands on whole 256 x 256 tiles (the direct-to-LDS kernel)."""
     got, want, pre, D = _run_gemm(m, n, k, layout, "bf16", dout, epi, seed=k)
     assert_close(got, want, D, TAU["bf16"], f"{layout} bf16->{dout} {m}x{n}x{k} {epi}")
+    _check_elementwise(got, _LAST["a"], _LAST["b"], layout == "TN", layout == "NT", _LAST["bias"], epi, dout,
+                       f"{layout} bf16->{dout} {m}x{n}x{k} {epi} per element")
     if epi == "bias_relu":
         bad, _ = mask_mismatch(got, pre, TAU["bf16"] * D)
         assert bad == 0
@@ -145,13 +160,16 @@ def test_matmul_bf16_whole_tiles(m, n, k, layout, dout, epi):
 
 @pytest.mark.parametrize("waves", [4, 8, 16])
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
-def test_matmul_bf16_every_wave_layout(layout, waves, monkeypatch):
-    """Every workgroup shape of the whole-tile kernel (the tuning override)."""
-    monkeypatch.setenv("TFD_BF16_WAVES", f"NN:{waves},NT:{waves},TN:{waves}")
-    got, want, _, D = _run_gemm(512, 768, 320, layout, "bf16", "bf16", "bias", seed=waves)
-    assert_close(got, want, D, TAU["bf16"], f"{layout} waves {waves}")
-    got, want, _, _ = _run_gemm(512, 256, 128, layout, "bf16", "f32", "none", kind="int")
-    assert_bits(got, want, f"integer {layout} waves {waves}")
+def test_matmul_bf16_every_wave_layout(layout, waves):
+    """Every workgroup shape of the whole-tile kernel (the tuning knob)."""
+    with T.tuning(bf16_waves_nn=waves, bf16_waves_nt=waves, bf16_waves_tn=waves):
+        got, want, _, D = _run_gemm(512, 768, 320, layout, "bf16", "bf16", "bias", seed=waves)
+        assert_close(got, want, D, TAU["bf16"], f"{layout} waves {waves}")
+        _check_elementwise(got, _LAST["a"], _LAST["b"], layout == "TN", layout == "NT", _LAST["bias"], "bias",
+                           "bf16", f"{layout} waves {waves} per element")
+        got, want, _, _ = _run_gemm(512, 256, 128, layout, "bf16", "f32", "none", kind="int")
+        assert_bits(got, want, f"integer {layout} waves {waves}")
+
 
 
 @pytest.mark.parametrize("layout", ["NN", "NT", "TN"])
@@ -398,20 +416,38 @@ def test_matmul_relu_grad_bias_add_grad(m, n, k, layout, dt, rounding):
     T.tfd_relu_grad_bias_add_grad(g, f, bp2, db2)
     torch.cuda.synchronize()
     assert torch.equal(bp, bp2), "backprops differ from MatMul + ReluGrad"
-    dy = to_f64(bp2)
+    # ReluGrad is an exact select: the fused dY is the oracle's ReluGrad of
+    # the plain MatMul's output, bit for bit
+    dy = to_f64(bp)
+    assert_bits(dy, oracle.relu_grad(to_f64(g), f_h), "fused dY = ReluGrad(plain MatMul output)")
     D = max(m, 1) * max(amax(dy), 1e-30)
     assert_close(to_f64(db), oracle.bias_add_grad(dy), D, TAU["f32"], "fused BiasAddGrad")
+    _check_colsum(to_f64(db), dy, "fused BiasAddGrad per column")
     # against the oracle's chain (mask decisions are exact here: features are given)
     store = "bf16t" if rounding == "truncate" else dt
     want = oracle.relu_grad(oracle.matmul(a_h, b_h, ta, tb, out=store), f_h)
     Dg = k * amax(a_h) * amax(b_h)
     assert_close(dy, want, Dg, TAU[dt], "fused dY")
+    if m > 0:
+        keep = f_h > 0
+        A, B = (a_h.T if ta else a_h), (b_h.T if tb else b_h)
+        exact = oracle.matmul(A, B, out="f64")
+        bound = product_bound(np.abs(A) @ np.abs(B), k, dy, store)
+        assert_elementwise(np.where(keep, dy, 0.0), np.where(keep, exact, 0.0), bound, "fused dY per element")
     # fixed summation order: a second call gives the same bits
     db3 = torch.empty_like(db)
     T.tfd_matmul_relu_grad_bias_add_grad(a, b, f, torch.empty_like(bp), db3, transpose_a=ta, transpose_b=tb,
                                          rounding=rounding)
     torch.cuda.synchronize()
     assert torch.equal(db, db3)
+
+
+def _check_colsum(db, dy, what):
+    """fp32 column sums of dy: within C_ACC * rows * u * sum |dy| + half an ulp."""
+    from tests.parity import C_ACC, U32, ulp
+    rows = dy.shape[0]
+    bound = C_ACC * rows * U32 * np.abs(dy).sum(axis=0) + 0.5 * ulp(db, "f32")
+    assert_elementwise(db, oracle.bias_add_grad(dy, out="f64"), bound, what)
 
 
 # ------------------------------------- fused output layer + squared error + BiasAddGrad
