@@ -205,6 +205,23 @@ TFD_API tfd_status tfd_relu_grad_bias_add_grad(const void* gradients, const void
                                        void* workspace, size_t workspace_bytes,
                                        void* stream);
 
+/*
+ * tfd_relu_grad_bias_add_grad for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments without the workspace, the same kernels
+ * and the same result bit for bit. The column partials go to a fixed device
+ * array inside the library instead (4 MiB per GPU, held until the process
+ * ends), so the call allocates nothing. Every call on a GPU uses that GPU's
+ * one array: calls that overlap in time on one GPU (other streams, other
+ * host threads) race and must not be issued. Shapes whose partials exceed
+ * the array return TFD_EINVAL (every shape up to at least 2^31 elements fits:
+ * the partials need at most about 2 MiB); TFD_EHIP if the array's address
+ * cannot be looked up on the current device.
+ */
+TFD_API tfd_status tfd_relu_grad_bias_add_grad_noalloc(const void* gradients, const void* features, void* backprops,
+                                                       float* bias_grad, int64_t rows, int64_t cols, tfd_dtype type,
+                                                       void* stream);
+
 /* Workspace bytes that tfd_matmul_relu_grad_bias_add_grad needs for an m x n output. */
 TFD_API size_t tfd_matmul_relu_grad_workspace_size(int64_t m, int64_t n, tfd_dtype type);
 

@@ -350,6 +350,32 @@ tfd_status tfd_relu_grad_bias_add_grad(const void* gradients, const void* featur
                     "tfd_relu_grad_bias_add_grad launch");
 }
 
+tfd_status tfd_relu_grad_bias_add_grad_noalloc(const void* gradients, const void* features, void* backprops,
+                                               float* bias_grad, int64_t rows, int64_t cols, tfd_dtype type,
+                                               void* stream) {
+  g_err[0] = 0;
+  const char* fn = "tfd_relu_grad_bias_add_grad_noalloc";
+  if (rows < 0 || cols < 0) return fail(TFD_EINVAL, "%s: negative size", fn);
+  if (!valid_dtype(type)) return fail(TFD_EINVAL, "%s: unknown element type", fn);
+  if (cols == 0) return TFD_OK;
+  if (!bias_grad) return fail(TFD_EINVAL, "%s: bias_grad is NULL", fn);
+  if (rows > 0 && !gradients) return fail(TFD_EINVAL, "%s: gradients is NULL", fn);
+  const size_t need = tfd::reduction_ws_bytes(rows, cols, type == TFD_BF16);
+  if (need > tfd::static_scratch_bytes())
+    return fail(TFD_EINVAL, "%s: %lld x %lld needs %zu bytes of scratch, above the fixed maximum of %zu", fn,
+                (long long)rows, (long long)cols, need, tfd::static_scratch_bytes());
+  const size_t bytes = (size_t)(rows * cols) * elem_bytes(type);
+  if (overlaps(backprops, bytes, gradients, bytes) || overlaps(backprops, bytes, features, bytes) ||
+      overlaps(bias_grad, (size_t)cols * 4, backprops, bytes))
+    return fail(TFD_EINVAL, "%s: overlapping buffers", fn);
+  void* ws = nullptr;
+  tfd_status st = hip_status(tfd::static_scratch(&ws), "tfd_relu_grad_bias_add_grad_noalloc scratch lookup");
+  if (st != TFD_OK) return st;
+  return hip_status(tfd::launch_relu_grad_bias_add_grad(gradients, features, backprops, bias_grad, rows, cols,
+                                                        type == TFD_BF16, ws, as_stream(stream)),
+                    "tfd_relu_grad_bias_add_grad_noalloc launch");
+}
+
 tfd_status tfd_bias_add_grad(const void* out_backprop, float* bias_grad, int64_t rows, int64_t cols,
                              tfd_dtype type, void* workspace, size_t workspace_bytes, void* stream) {
   tfd_status st = tfd_relu_grad_bias_add_grad(out_backprop, nullptr, nullptr, bias_grad, rows, cols, type,

@@ -84,6 +84,11 @@ size_t reduction_ws_bytes(int64_t rows, int64_t cols, bool bf16);
 hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* out, float* db,
                                           int64_t rows, int64_t cols, bool bf16, void* ws,
                                           hipStream_t s);
+// The device array that the no-allocation entry point uses instead of a
+// workspace: its capacity, and its address on the current device (looked up
+// once per device).
+size_t static_scratch_bytes();
+hipError_t static_scratch(void** out);
 // The same with the Relu test read from a bit mask (rows x ldm words).
 hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,
                                                float* db, int64_t rows, int64_t cols, bool bf16, void* ws,

@@ -13,6 +13,8 @@
 // column in row-chunk order. The grid depends only on (rows, cols, type), so
 // the bits of the result do not change from call to call.
 
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -347,6 +349,39 @@ hipError_t launch_relu_mask(const void* x, int64_t ldx, uint32_t* mask, int64_t 
                          mask, ldm, rows, cols);
   }
   return hipGetLastError();
+}
+
+// Scratch of the entry point that allocates nothing
+// (tfd_relu_grad_bias_add_grad_noalloc): the column partials of pass 1 live in
+// this file-scope device array instead of a caller's workspace. Each GPU the
+// library runs on holds its own copy until the process ends. In host code the
+// array's name is not a device address: its address on a device comes from
+// hipGetSymbolAddress, looked up once per device with that device current,
+// and only that address is passed to kernels.
+constexpr size_t kStaticScratchBytes = size_t(4) << 20;
+static __device__ __align__(256) float scratch[kStaticScratchBytes / sizeof(float)];
+
+size_t static_scratch_bytes() { return kStaticScratchBytes; }
+
+hipError_t static_scratch(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace tfd

@@ -37,7 +37,7 @@ EXPORTS = (
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
     "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
     "tfd_matmul_relu_mask_grad_bias_add_grad", "tfd_matmul_workspace_size", "tfd_matmul_with_workspace",
-    "tfd_set_tuning",
+    "tfd_set_tuning", "tfd_relu_grad_bias_add_grad_noalloc",
 )
 
 
@@ -99,6 +99,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "tfd_matmul_relu_mask_grad_bias_add_grad": ([i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, i32, i32,
                                                      vp, sz, vp], i32),
         "tfd_set_tuning": ([ctypes.c_char_p, i32], i32),
+        "tfd_relu_grad_bias_add_grad_noalloc": ([vp, vp, vp, vp, i64, i64, i32, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -405,6 +406,23 @@ def tfd_relu_grad_bias_add_grad(gradients, features, backprops, bias_grad, works
     _check(load().tfd_relu_grad_bias_add_grad(_ptr(gradients), _ptr(features), _ptr(backprops), _ptr(bias_grad),
                                               rows, cols, _dtype(gradients), _ptr(ws), ws.numel(),
                                               _stream(stream)))
+    return backprops, bias_grad
+
+
+def tfd_relu_grad_bias_add_grad_noalloc(gradients, features, backprops, bias_grad, stream=None):
+    """tfd_relu_grad_bias_add_grad without a workspace: the library's fixed
+    device scratch holds the partials, so nothing is allocated (for callers
+    that cannot allocate; calls that overlap on one GPU race)."""
+    rows, cols = gradients.shape
+    _flat(gradients, "gradients")
+    for t, name in ((features, "features"), (backprops, "backprops")):
+        if t is not None and (not t.is_contiguous() or t.dtype != gradients.dtype or t.shape != gradients.shape):
+            raise ValueError(f"{name} must be contiguous and match gradients")
+    if bias_grad.dtype != torch.float32 or bias_grad.numel() != cols or not bias_grad.is_contiguous():
+        raise ValueError("bias_grad must be a contiguous fp32 vector of length cols")
+    _check(load().tfd_relu_grad_bias_add_grad_noalloc(_ptr(gradients), _ptr(features), _ptr(backprops),
+                                                      _ptr(bias_grad), rows, cols, _dtype(gradients),
+                                                      _stream(stream)))
     return backprops, bias_grad
 
 
