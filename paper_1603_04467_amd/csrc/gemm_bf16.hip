@@ -143,6 +143,78 @@ __device__ __forceinline__ uint2 ds_read_tr16_b64(const char* p) {
 }
 __device__ __forceinline__ void frag_wait(u32x4& f) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f)); }
 
+// Building blocks of the scheduled 4-wave k loop (one wave per SIMD). Its LDS
+// reads are inline assembly, so that the compiler inserts no waits of its own
+// for them; the loop waits explicitly (wait_lds). Its MFMAs are the builtin,
+// fenced on both sides by scheduling barriers, so that they stay exactly
+// where they are written among the reads and copies while the compiler still
+// knows them for what they are: it inserts the wait states an MFMA needs
+// around its operands and results, also where it copies accumulators between
+// registers at the joins of the loop and its peeled tail (an MFMA written as
+// inline assembly gets none, and such a copy then reads a result the matrix
+// core has not yet written).
+// LDS reads into a fragment register tuple that is tied to its previous
+// contents ("+v"), so the compiler keeps every fragment buffer in the same
+// registers for the whole loop and never points a read at registers that an
+// MFMA issued just before still has to read.
+template <int IMM>
+__device__ __forceinline__ void ds_read_b128_into(u32x4& v, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "+v"(v) : "v"(addr), "i"(IMM));
+}
+// The two transposing reads of an m/n-contiguous fragment, into the low and
+// high halves (k 0-3 and 4-7 of the lane's eight).
+template <int IMM0, int IMM1>
+__device__ __forceinline__ void ds_read_tr_pair_into(uint2& lo, uint2& hi, uint32_t addr) {
+  asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%3\n\tds_read_b64_tr_b16 %1, %2 offset:%4"
+               : "+v"(lo), "+v"(hi)
+               : "v"(addr), "i"(IMM0), "i"(IMM1));
+}
+// f(integral_constant<int, I>) for I = 0 .. N-1, unrolled at compile time.
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+// 32 x 32 x 16 MFMA, pinned in place by scheduling barriers.
+__device__ __forceinline__ void mfma_acc(f32x16& acc, const u32x4& a, const u32x4& b) {
+  __builtin_amdgcn_sched_barrier(0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
+                                               0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+}
+// Fragment buffer of one operand for one k-step (4 fragments of 32 rows or
+// columns): a k-contiguous operand's fragment is one 16-byte LDS read, an
+// m/n-contiguous one's two 8-byte transposing reads (low and high halves).
+template <bool KC> struct FragBuf;
+template <> struct FragBuf<true> {
+  u32x4 f[4];
+  template <int I>
+  __device__ __forceinline__ u32x4 get() const { return f[I]; }
+  // Wait for every outstanding LDS read; tie the registers to the wait so
+  // that nothing reads them before their data arrived.
+  __device__ __forceinline__ void tie() { asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3])); }
+};
+template <> struct FragBuf<false> {
+  uint2 lo[4], hi[4];
+  template <int I>
+  __device__ __forceinline__ u32x4 get() const { return u32x4{lo[I].x, lo[I].y, hi[I].x, hi[I].y}; }
+  __device__ __forceinline__ void tie() {
+    asm volatile("" : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]),
+                 "+v"(hi[3]));
+  }
+};
+template <typename FA, typename FB>
+__device__ __forceinline__ void wait_lds(FA& a, FB& b, bool vm) {
+  if (vm)
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+  else
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  a.tie();
+  b.tie();
+}
+
 // Fragment of 32 rows (A) or 32 columns (B) starting at `base`, k-step q.
 template <bool KC>
 __device__ __forceinline__ u32x4 read_frag(const char* tile, int base, int q, int lane) {
@@ -262,6 +334,192 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   // this workgroup's k-tiles: kt0 .. kt0 + kt_count - 1
   const int kt0 = split * p.kt_per;
   const int kt_count = min(p.k / kBK - kt0, p.kt_per);
+  if constexpr (kWavesM * kWavesN == 4 && A_KC && B_KC) {
+    // One wave per SIMD (128 x 128 wave tiles: 128 KiB of fragment reads per
+    // k-tile instead of 192 KiB with 8 waves). A single wave must keep its
+    // matrix core busy, so the schedule is explicit: in every k-step, one LDS
+    // read of the next k-step's fragments after each of the first 8 MFMAs
+    // (their latency then hides behind the last 8), and the copies of the
+    // next k-tile spread one pair per two MFMAs over the second half of
+    // k-step 3 of the previous k-tile and of k-step 0. The k-tile barrier
+    // sits after k-step 2: by then every wave holds k-step 3's fragments in
+    // registers and its copies of the next k-tile have landed, so k-step 3's
+    // MFMAs run behind the barrier while the next k-tile's first fragments are
+    // read and the copies of the k-tile after it start into the stage just
+    // released. Everything that varies per copy or read is a scalar or an
+    // immediate: copies take a wave-uniform base address (SGPRs) plus a
+    // per-lane 32-bit offset fixed for the whole loop, and the loop is
+    // unrolled over the two LDS stages, whose offsets become immediates.
+    // LDS: A of stage s at s * 32 KiB, B of stage s at 64 KiB + s * 32 KiB.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform: LDS bases go to M0 directly
+    uint32_t offa[8], offb[8];  // per-lane byte offsets of copy instruction j, both operands
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int blk = wv * 8 + j;
+      if constexpr (A_KC) {
+        const int r = blk * 8 + (lane >> 3);
+        offa[j] = (uint32_t)(((int64_t)r * p.lda + (((lane & 7) ^ swz_kc(r)) * 8)) * 2);
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        offa[j] = (uint32_t)(((int64_t)kr * p.lda + (((lane & 31) ^ swz_mn(kr)) * 8)) * 2);
+      }
+      if constexpr (B_KC) {
+        const int r = blk * 8 + (lane >> 3);
+        offb[j] = (uint32_t)(((int64_t)r * p.ldb + (((lane & 7) ^ swz_kc(r)) * 8)) * 2);
+      } else {
+        const int kr = blk * 2 + (lane >> 5);
+        offb[j] = (uint32_t)(((int64_t)kr * p.ldb + (((lane & 31) ^ swz_mn(kr)) * 8)) * 2);
+      }
+    }
+    // wave-uniform operand base of k-tile kt (absolute)
+    auto abase = [&](int kt_abs) -> const char* {
+      return reinterpret_cast<const char*>(A_KC ? p.a + (int64_t)m0 * p.lda + (int64_t)kt_abs * kBK
+                                                : p.a + (int64_t)kt_abs * kBK * p.lda + m0);
+    };
+    auto bbase = [&](int kt_abs) -> const char* {
+      return reinterpret_cast<const char*>(B_KC ? p.b + (int64_t)n0 * p.ldb + (int64_t)kt_abs * kBK
+                                                : p.b + (int64_t)kt_abs * kBK * p.ldb + n0);
+    };
+    auto a_lds = [&](int stage) { return smem + stage * kOperandBytes; };
+    auto b_lds = [&](int stage) { return smem + 2 * kOperandBytes + stage * kOperandBytes; };
+    auto copy_pair = [&](const char* ga, const char* gb, int stage, int j) {
+      // the empty asm keeps the 32-bit offsets from being widened outside the
+      // loop, so that the copies use the scalar-base form (SGPR pair + VGPR)
+      uint32_t oa = offa[j], ob = offb[j];
+      asm("" : "+v"(oa), "+v"(ob));
+      __builtin_amdgcn_global_load_lds(ga + oa, (lds_void*)(a_lds(stage) + (wv * 8 + j) * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gb + ob, (lds_void*)(b_lds(stage) + (wv * 8 + j) * 1024), 16, 0, 0);
+    };
+    // Per-lane LDS read addresses of stage 0; the stage, the k-step and the
+    // fragment index enter as immediate offsets where the layout allows.
+    // k-contiguous operand (256 rows of 128 B, chunk c of row r at slot
+    // c ^ swz_kc(r)): fragment i of k-step q reads row R + 32 i; rows 64
+    // apart share the swizzle, so an address per (q, i mod 2) and +8 KiB per
+    // two fragments. m/n-contiguous operand (64 k-rows of 512 B): the k-step
+    // and the half of the transposing pair move the k-row by 8 q + 4 s, an
+    // immediate; an address per fragment.
+    const int half = lane >> 5;
+    auto kc_addr = [&](const char* base_lds, int wbase, int q, int par) -> uint32_t {
+      const int r = wbase + par * 32 + (lane & 31);
+      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + r * 128 + (((half * 4 + q) ^ swz_kc(r)) << 4)));
+    };
+    auto mn_addr = [&](const char* base_lds, int wbase, int j) -> uint32_t {
+      const int g = lane >> 4, lr = lane & 15;
+      const int mn = wbase + j * 32 + 16 * (g & 1) + 4 * (lr & 3);
+      const int kr0 = 32 * half + (lr >> 2);
+      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + kr0 * 512 + (((mn >> 3) ^ swz_mn(kr0)) << 4) + (mn & 7) * 2));
+    };
+    uint32_t ra[8], rb[8];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      ra[x] = A_KC ? kc_addr(a_lds(0), wm * kWTM, x >> 1, x & 1) : (x < 4 ? mn_addr(a_lds(0), wm * kWTM, x) : 0u);
+      rb[x] = B_KC ? kc_addr(b_lds(0), wn * kWTN, x >> 1, x & 1) : (x < 4 ? mn_addr(b_lds(0), wn * kWTN, x) : 0u);
+    }
+    // read fragment F (0..3) of an operand, k-step Q of stage S, into a buffer
+    auto read_frag_into = [&](auto f_tag, auto q_tag, auto s_tag, auto& buf, const uint32_t (&ra_)[8]) {
+      constexpr int F = decltype(f_tag)::value, Q = decltype(q_tag)::value, S = decltype(s_tag)::value;
+      if constexpr (std::is_same<std::decay_t<decltype(buf)>, FragBuf<true>>::value)
+        ds_read_b128_into<(F >> 1) * 8192 + S * kOperandBytes>(buf.f[F], ra_[Q * 2 + (F & 1)]);
+      else
+        ds_read_tr_pair_into<(8 * Q) * 512 + S * kOperandBytes, (8 * Q + 4) * 512 + S * kOperandBytes>(
+            buf.lo[F], buf.hi[F], ra_[F]);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    FragBuf<A_KC> fa0, fa1;
+    FragBuf<B_KC> fb0, fb1;
+    // Read slot r (after MFMA r of a k-step) fills fragment kSlot[r] of A
+    // (< 4) or B (>= 4) for the next k-step. The order keeps at least 6 MFMAs
+    // between an MFMA's last read of a fragment register (A fragment i: MFMA
+    // 4 i + 3 of the previous k-step, B fragment j: MFMA 12 + j) and the LDS
+    // read that overwrites it.
+    // slots: A0, A1, B0, A2, B1, B2, A3, B3
+    // k-step: 16 MFMAs on (fa, fb); after MFMA r < 8 the read of slot r of the
+    // next k-step's fragments (k-step RQ of stage RS; kRead), after MFMAs 8,
+    // 10, 12, 14 one copy pair (kCopy)
+    auto kstep = [&](auto read_tag, auto copy_tag, auto rq_tag, auto rs_tag, auto& fa, auto& fb, auto& na, auto& nb,
+                     const char* ga, const char* gb, int cstage, int cp_half) {
+      constexpr bool kRead = decltype(read_tag)::value, kCopy = decltype(copy_tag)::value;
+      static_for<16>([&](auto i_tag) {
+        constexpr int i = decltype(i_tag)::value;
+        mfma_acc(acc[i >> 2][i & 3], fa.template get<(i >> 2)>(), fb.template get<(i & 3)>());
+        if constexpr (kRead && i < 8) {
+          constexpr int kSlot[8] = {0, 1, 4, 2, 5, 6, 3, 7};
+          constexpr int sl = kSlot[i];
+          if constexpr (sl < 4)
+            read_frag_into(std::integral_constant<int, sl>{}, rq_tag, rs_tag, na, ra);
+          else
+            read_frag_into(std::integral_constant<int, sl - 4>{}, rq_tag, rs_tag, nb, rb);
+        }
+        if constexpr (kCopy && i >= 8 && (i & 1) == 0) copy_pair(ga, gb, cstage, 4 * cp_half + ((i - 8) >> 1));
+      });
+    };
+    using Q0 = std::integral_constant<int, 0>;
+    using Q1 = std::integral_constant<int, 1>;
+    using Q2 = std::integral_constant<int, 2>;
+    using Q3 = std::integral_constant<int, 3>;
+    // One k-tile in stage S. kMore: a next k-tile exists (copy its second
+    // half in k-step 0, read its first fragments in k-step 3); kMore2: the
+    // one after it too (copy its first half in k-step 3).
+    auto ktile = [&](auto stage_tag, auto more_tag, auto more2_tag, int kt) {
+      constexpr int S = decltype(stage_tag)::value;
+      using SN = std::integral_constant<int, 1 - S>;
+      using M1 = std::integral_constant<bool, decltype(more_tag)::value>;
+      using M2 = std::integral_constant<bool, decltype(more2_tag)::value>;
+      const char* ga1 = abase(kt0 + kt + 1);
+      const char* gb1 = bbase(kt0 + kt + 1);
+      kstep(T_{}, M1{}, Q1{}, stage_tag, fa0, fb0, fa1, fb1, ga1, gb1, 1 - S, 1);
+      wait_lds(fa1, fb1, false);
+      kstep(T_{}, F_{}, Q2{}, stage_tag, fa1, fb1, fa0, fb0, ga1, gb1, 1 - S, 0);
+      wait_lds(fa0, fb0, false);
+      kstep(T_{}, F_{}, Q3{}, stage_tag, fa0, fb0, fa1, fb1, ga1, gb1, 1 - S, 0);
+      // the k-tile barrier: k-step 3's fragments are in registers, this
+      // wave's copies of the next k-tile have landed
+      wait_lds(fa1, fb1, true);
+      __builtin_amdgcn_s_barrier();
+      kstep(M1{}, M2{}, Q0{}, SN{}, fa1, fb1, fa0, fb0, abase(kt0 + kt + 2), bbase(kt0 + kt + 2), S, 0);
+      // The next k-tile's first fragments are waited for here, at the end of
+      // the k-tile and not at the start of the next: no read is in flight
+      // across a branch, where the compiler may move registers around.
+      wait_lds(fa0, fb0, false);
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    // prologue: k-tile 0 in stage 0, its first fragments, and the first half
+    // of k-tile 1's copies into stage 1
+#pragma unroll
+    for (int j = 0; j < 8; ++j) copy_pair(abase(kt0), bbase(kt0), 0, j);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    static_for<4>([&](auto f_tag) {
+      read_frag_into(f_tag, Q0{}, S0{}, fa0, ra);
+      read_frag_into(f_tag, Q0{}, S0{}, fb0, rb);
+    });
+    if (kt_count > 1) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) copy_pair(abase(kt0 + 1), bbase(kt0 + 1), 1, j);
+    }
+    wait_lds(fa0, fb0, false);
+    // steady state, two k-tiles (both stages) per trip without conditions,
+    // then the last one to three k-tiles (kt even: stage 0 first)
+    int kt = 0;
+    for (; kt + 3 < kt_count; kt += 2) {
+      ktile(S0{}, T_{}, T_{}, kt);
+      ktile(S1{}, T_{}, T_{}, kt + 1);
+    }
+    const int rest = kt_count - kt;
+    if (rest == 3) {
+      ktile(S0{}, T_{}, T_{}, kt);
+      ktile(S1{}, T_{}, F_{}, kt + 1);
+      ktile(S0{}, F_{}, F_{}, kt + 2);
+    } else if (rest == 2) {
+      ktile(S0{}, T_{}, F_{}, kt);
+      ktile(S1{}, F_{}, F_{}, kt + 1);
+    } else {
+      ktile(S0{}, F_{}, F_{}, kt);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+  } else {
   copy_tile<A_KC, kThreads>(p.a, p.lda, m0, kt0 * kBK, smem, wave, lane);
   copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, kt0 * kBK, smem + kOperandBytes, wave, lane);
   __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) lgkmcnt(0)
@@ -319,6 +577,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
       for (int j = 0; j < kFN; ++j) fb[0][j] = read_frag<B_KC>(nx + kOperandBytes, wn * kWTN + j * 32, 0, lane);
     }
   }
+  }  // k loop of 8 or 16 waves
 
   if constexpr (!kEarlyBias) load_bias();
   const bool trunc16 = (p.epi & kEpiTrunc16) != 0;
@@ -581,7 +840,8 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
 // Waves per workgroup: 4 (2x2 of 128x128), 8 (2x4 of 128x64) or 16 (4x4 of 64x64).
 template <bool A_KC, bool B_KC>
 hipError_t launch_waves(const GemmDesc& d, int waves, hipStream_t s) {
-  if (waves == 4) return launch<A_KC, B_KC, 2, 2>(d, s);
+  // the 4-wave loop keeps per-lane copy offsets below 2^31 bytes
+  if (waves == 4 && d.lda < (1 << 22) && d.ldb < (1 << 22)) return launch<A_KC, B_KC, 2, 2>(d, s);
   if (waves == 16) return launch<A_KC, B_KC, 4, 4>(d, s);
   return launch<A_KC, B_KC, 2, 4>(d, s);
 }
@@ -674,11 +934,18 @@ bool gemm_bf16_256_ok(const GemmDesc& d) {
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // A is k-contiguous unless transposed; B is k-contiguous when transposed.
-  // Defaults measured inside the training step: 8 waves (2 per SIMD) for
-  // NN and NT, 16 waves for TN, whose two transposing-read operands gain most
-  // from more waves to hide LDS latency.
+  // Defaults measured on the step's shapes: 8 waves (2 per SIMD) for NN, 16
+  // for TN, whose two transposing-read operands gain most from more waves to
+  // hide LDS latency; for NT the scheduled 4-wave loop over a long k range
+  // (forward and input-gradient products of the 4096-wide layers), except
+  // under the ReluGrad epilogues, whose feature or mask reads cost the 4-wave
+  // epilogue more than its loop saves; 8 waves otherwise.
   if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, 8), s);
-  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, 8), s);
+  if (!d.ta && d.tb) {
+    const bool long_k = d.k >= 2048 && d.splits <= 1;
+    const bool relu_grad = d.mask_in != nullptr || d.features != nullptr;
+    return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, long_k && !relu_grad ? 4 : 8), s);
+  }
   return launch_gemm_bf16_256_tn(d, s);
 }
 #endif
