@@ -7,23 +7,42 @@ Prints ONE JSON line. The headline workload is the 4-layer, 4096-wide MLP
 with 16-bit activations/weights, fp32 accumulation and fp32 master weights,
 batch 16384 ("wide4096x4-bf16"); its fp32 twin at batch 8192
 ("wide4096x4-f32"), the truncating 16-bit variant, the tall 512 -> 32768 layer
-and the MNIST-shaped steps are timed in the same run and reported under "also".
+and the MNIST-shaped steps are timed in the same run and reported under
+"also"; the per-replica GEMM shapes of an 8-way batch split under
+"per_replica".
 
-Timing: every step starts from the same Variables (a stream-ordered restore
-before the step's start event), so each timed step is exactly the computation
-the parity tests check. ms_per_step is the mean of the per-step HIP event
-intervals on the launch stream; the host-side bracket (synchronize on both
-sides of the K steps, restores included) is reported as wall_ms_per_step.
-Throughput counts the step's GEMM FLOPs, sum of 2*m*n*k.
-The cpu_baseline leg times the oracle (float64 numpy) on a row slice of the
-same workload on the host cores.
+Timing. Inputs are generated once and stay resident in HBM. Every step
+starts from the same Variables (a stream-ordered restore before the step's
+start event), so each timed step is exactly the computation the parity tests
+check. Per workload:
+  1. W warm-up steps;
+  2. a per-op pass (K steps, a HIP event between every two launches) that
+     gives the per-op breakdown and picks the dominant kernel: the GEMM
+     kernel variant (layout, fused epilogue, shape) with the most time per
+     step;
+  3. the timed pass (K steps): HIP events at the step boundaries and around
+     each launch of the dominant kernel only, on the launch stream.
+     ms_per_step is the mean step interval, value = GEMM FLOPs per step
+     (sum of 2 m n k) / ms_per_step; roofline.achieved = the dominant
+     kernel's FLOPs per launch / its mean launch interval in this pass.
+The MNIST-shaped steps are launch-bound: their value comes from the fastest
+of four unmarked launch modes (one stream, several streams, HIP graph
+replay of either).
+
+The cpu_baseline leg times the oracle (float64 numpy) on bounded row samples
+of every workload on the host cores, and compares the oracle's row-local
+outputs (H, G, dY, dX) on those rows with the GPU's from the timed pass
+(parity ratios max|err| / D, ReLU decisions inside the rounding band).
 """
 
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -40,20 +59,16 @@ PRIMARY = "wide4096x4-bf16"
 # steps too small to fill the GPU with one kernel at a time: also timed with
 # concurrent streams and HIP graph replay
 LAUNCH_BOUND = ("mlp784-1024-1024-10-xent", "mlp784-1024-1024-10", "dense784x100")
-# timed in the same run and reported under "also": the fp32 twin, the truncating
-# 16-bit variant, the tall 512 -> 32768 layer (given upstream gradient, no update),
-# then the MNIST-shaped steps (classifier head and squared-error head) and the single layer
 SECONDARY = ("wide4096x4-f32", "wide4096x4-bf16-trunc", "tall512x32768-bf16", "mlp784-1024-1024-10-xent",
              "mlp784-1024-1024-10", "dense784x100")
+# oracle samples (batch rows) per workload: bounded CPU work, about 15 s in all
+CPU_ROWS = {"wide4096x4-bf16": 4096, "wide4096x4-f32": 2048, "tall512x32768-bf16": 2048,
+            "mlp784-1024-1024-10": None, "dense784x100": None}
+KERNEL_SOURCES = {"bf16": "paper_1603_04467_amd/csrc/gemm_bf16.hip", "f32": "paper_1603_04467_amd/csrc/gemm.hip"}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.md")
 
 
-def _gemm_bytes(shape, layout, eb):
-    """Compulsory HBM bytes of one GEMM: read A and B once, write C once
-    (the weight gradient is written in fp32)."""
-    m, n, k = shape
-    out = 4 if layout == "TN" else eb
-    return m * k * eb + k * n * eb + m * n * out
-
+# ----------------------------------------------------------------- kernels
 
 def _op_kind(name: str) -> str:
     for p in ("fwd", "dx", "dw", "relugrad", "sgd", "loss"):
@@ -62,7 +77,109 @@ def _op_kind(name: str) -> str:
     return name
 
 
-def time_workload(name: str, steps: int, warmup: int):
+def op_info(s, tag):
+    """What the launch of op `tag` computes: for GEMMs the layout, fused
+    epilogue, shape and FLOPs (and a kernel id shared by every launch of the
+    same kernel variant), for the memory-bound ops their compulsory bytes."""
+    from paper_1603_04467_amd import tfdense as T
+    from paper_1603_04467_amd.step import fused_below, fused_top
+
+    w = s.w
+    kind = _op_kind(tag)
+    l = int(tag[len(kind):]) - 1 if tag[len(kind):].isdigit() else None
+    eb = 2 if w.act == "bf16" else 4
+    N, L = w.batch, w.layers
+    d = {"kind": kind}
+    if kind in ("fwd", "dx", "dw"):
+        if kind == "fwd":
+            m, n, k, lay = N, w.dims[l + 1], w.dims[l], s.forward_layout
+            if l == L - 1 and fused_top(w, s.fuse):
+                epi = "bias+sq_err+colsum"
+            elif s.masks[l] is not None:
+                epi = "bias_relu+mask"
+            else:
+                epi = "bias_relu" if w.relus[l] else "bias"
+        elif kind == "dx":
+            m, n, k, lay = N, w.dims[l], w.dims[l + 1], "NT"
+            if fused_below(w, l, s.fuse):
+                epi = "relugrad_mask+colsum" if s.masks[l - 1] is not None else "relugrad+colsum"
+            else:
+                split = T.tfd_matmul_workspace_size(m, n, k, s.act, s.act, transpose_b=True) > 0
+                epi = "splitk" if split else "none"
+        else:
+            m, n, k, lay = w.dims[l], w.dims[l + 1], N, "TN"
+            epi = "none"
+        out = "f32" if kind == "dw" else w.act
+        d.update(layout=lay, epi=epi, shape=[m, n, k], flops=2 * m * n * k,
+                 kernel=f"gemm {w.act} {lay} {epi} {m}x{n}x{k} -> {out}",
+                 algorithmic_bytes=m * k * eb + k * n * eb + m * n * (4 if out == "f32" else eb))
+    elif kind == "relugrad":
+        M = w.dims[l + 1]
+        if not w.relus[l]:
+            byt = N * M * eb + 4 * M                 # BiasAddGrad alone
+        elif s.use_masks:
+            byt = 2 * N * M * eb + N * M // 8 + 4 * M  # gradient and 1-bit mask in, dY out
+        else:
+            byt = 3 * N * M * eb + 4 * M             # gradient and features in, dY out
+        d["bytes"] = byt
+    elif kind == "sgd":
+        K, M = w.dims[l], w.dims[l + 1]
+        d["bytes"] = K * M * (12 + (4 if w.masters else 0)) + 12 * M
+    elif kind == "loss":
+        d["bytes"] = 3 * N * w.dims[-1] * eb if w.cost != "xent" else 2 * N * w.dims[-1] * eb + 4 * N
+    return d
+
+
+# ----------------------------------------------------------------- clock
+
+def _clock_probe_mhz(counters):
+    c = counters.cpu().numpy()
+    return [100.0 * float(r[0]) / float(r[1]) for r in c if r[1] > 0]
+
+
+def sample_clock(s, probes: int = 8, iterations: int = 500_000):
+    """Engine clock in MHz, from tfd_clock_probe (shader clock cycles over
+    100 MHz real-time ticks in one wave): `probes` probes on a second stream
+    while step `s` runs back to back on the launch stream (restored Variables,
+    as in the timed pass), and as many with the GPU otherwise idle."""
+    import torch
+
+    from paper_1603_04467_amd import tfdense as T
+
+    side = torch.cuda.Stream()
+    loaded = torch.zeros(probes, 3, dtype=torch.int64, device="cuda")
+    idle = torch.zeros(probes, 3, dtype=torch.int64, device="cuda")
+    for i in range(probes):
+        T.tfd_clock_probe(idle[i], iterations)
+    torch.cuda.synchronize()
+    for i in range(probes):
+        s.restore()
+        s.run()
+        side.wait_stream(torch.cuda.current_stream())
+        s.restore()
+        s.run()
+        with torch.cuda.stream(side):
+            T.tfd_clock_probe(loaded[i], iterations)
+        s.restore()
+        s.run()
+    torch.cuda.synchronize()
+
+    def stats(v):
+        return {"median": round(float(np.median(v)), 1), "min": round(float(np.min(v)), 1),
+                "max": round(float(np.max(v)), 1), "probes": len(v)} if v else None
+    return {"under_load": stats(_clock_probe_mhz(loaded)), "idle": stats(_clock_probe_mhz(idle)),
+            "source": "tfd_clock_probe: 100 * s_memtime cycles / s_memrealtime ticks of one wave; under_load "
+                      "on a second stream while the step runs"}
+
+
+# ----------------------------------------------------------------- timing
+
+def _event():
+    import torch
+    return torch.cuda.Event(enable_timing=True)
+
+
+def time_workload(name: str, steps: int, warmup: int, keep_rows: int = 0, clock: bool = False):
     import torch
 
     from paper_1603_04467_amd import workloads
@@ -72,96 +189,85 @@ def time_workload(name: str, steps: int, warmup: int):
     inp = workloads.generate(w, seed=0)
     s = DenseStep(w, inp)
     stream = torch.cuda.current_stream()
+    tags = [n.name for n in s.nodes()]
+    info = {t: op_info(s, t) for t in tags}
 
     for _ in range(warmup):
         s.restore()
         s.run()
     torch.cuda.synchronize()
 
-    # per-step and per-op events, recorded on the launch stream
-    step_ev = []
+    # per-op pass: an event between every two launches
     op_ev = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
     for _ in range(steps):
         s.restore()
         marks = []
 
         def mark(tag, marks=marks):
-            e = torch.cuda.Event(enable_timing=True)
+            e = _event()
             e.record(stream)
             marks.append((tag, e))
 
         s.run(mark=mark)
-        step_ev.append((marks[0][1], marks[-1][1]))
         op_ev.append(marks)
     torch.cuda.synchronize()
-    wall = (time.perf_counter() - t0) / steps * 1e3
-
-    step_ms = [a.elapsed_time(b) for a, b in step_ev]
     per_op = {}
     for marks in op_ev:
         for (tag, e0), (_, e1) in zip(marks[:-1], marks[1:]):
             per_op.setdefault(tag, []).append(e0.elapsed_time(e1))
-    ms = float(np.mean(step_ms))
-    pct = {f"p{q}": round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)}
-    flops = w.flops()
-    tflops = flops / (ms * 1e-3) / 1e12
-
-    # per-op summary: mean ms, and FLOP/s or bytes/s against the roofline
-    gemm_shapes = w.gemm_shapes()
-    L = w.layers
-    eb = 2 if w.act == "bf16" else 4
-    N = w.batch
     ops = {}
-    for tag, v in per_op.items():
-        kind = _op_kind(tag)
-        l = int(tag[len(kind):]) if tag[len(kind):].isdigit() else None
-        d = {"ms": float(np.mean(v))}
-        if kind in ("fwd", "dx", "dw"):
-            if kind == "fwd":
-                m, n, k, lay = gemm_shapes[l - 1]
-                lay = s.forward_layout
-            else:
-                idx = L + 2 * (L - l) + (0 if kind == "dx" else 1)
-                m, n, k, lay = gemm_shapes[idx]
-            f = 2 * m * n * k
-            d.update(layout=lay, shape=[m, n, k], flops=f, tflops=f / (d["ms"] * 1e-3) / 1e12)
-        elif kind == "relugrad":
-            M = w.dims[l]
-            if not w.relus[l - 1]:
-                byt = N * M * eb + 4 * M                 # BiasAddGrad alone
-            elif s.use_masks:
-                byt = 2 * N * M * eb + N * M // 8 + 4 * M  # gradient and 1-bit mask in, dY out
-            else:
-                byt = 3 * N * M * eb + 4 * M             # gradient and features in, dY out
-            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
-        elif kind == "sgd":
-            K, M = w.dims[l - 1], w.dims[l]
-            # fp32 var and delta read, var written; with fp32 masters also the
-            # 16-bit copy and its transpose (2 + 2 bytes); the bias update
-            byt = K * M * (12 + (4 if w.masters else 0)) + 12 * M
-            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
-        elif kind == "loss":
-            # squared error: output and target read, gradient written;
-            # cross-entropy: logits read, gradient written, one label per row
-            byt = 3 * N * w.dims[-1] * eb if w.cost != "xent" else 2 * N * w.dims[-1] * eb + 4 * N
-            d.update(bytes=byt, gbs=byt / (d["ms"] * 1e-3) / 1e9)
+    for tag in tags:
+        d = dict(info[tag])
+        d["ms"] = float(np.mean(per_op[tag]))
+        if "flops" in d:
+            d["tflops"] = d["flops"] / (d["ms"] * 1e-3) / 1e12
+        if "bytes" in d:
+            d["gbs"] = d["bytes"] / (d["ms"] * 1e-3) / 1e9
         ops[tag] = d
 
-    # dominant kernel: the GEMM layout with the most total time
-    by_layout = {}
+    # dominant kernel: the GEMM kernel variant with the most time per step
+    by_kernel = {}
     for tag, d in ops.items():
-        if "layout" in d:
-            by_layout.setdefault(d["layout"], []).append(d)
-    dom_layout, dom = max(by_layout.items(), key=lambda kv: sum(x["ms"] for x in kv[1]))
-    dom_ms = float(np.mean([x["ms"] for x in dom]))
-    dom_flops = dom[0]["flops"]
-    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+        if "kernel" in d:
+            by_kernel.setdefault(d["kernel"], []).append(tag)
+    dom_kernel, dom_tags = max(by_kernel.items(), key=lambda kv: sum(ops[t]["ms"] for t in kv[1]))
+
+    # timed pass: step boundaries and the dominant kernel's launches only
+    step_ev, dom_ev = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        s.restore()
+        open_ = []
+
+        def mark(tag, open_=open_):
+            if open_:
+                e = _event()
+                e.record(stream)
+                dom_ev.append((open_.pop(), e))
+            if tag in dom_tags:
+                e = _event()
+                e.record(stream)
+                open_.append(e)
+
+        a, b = _event(), _event()
+        a.record(stream)
+        s.run(mark=mark)
+        b.record(stream)
+        step_ev.append((a, b))
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps * 1e3
+    step_ms = [a.elapsed_time(b) for a, b in step_ev]
+    dom_ms = [a.elapsed_time(b) for a, b in dom_ev]
+    ms = float(np.mean(step_ms))
+    pct = {f"p{q}": round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)}
+    tflops = w.flops() / (ms * 1e-3) / 1e12
+    dom = info[dom_tags[0]]
+    dom_mean = float(np.mean(dom_ms))
+    achieved = dom["flops"] / (dom_mean * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.act]
-    kernel_name = f"gemm_{dom_layout}_{w.act}"
-    traffic = lookup_traffic(kernel_name, dom[0]["shape"], w.act)
-    return {
+    traffic = lookup_traffic(dom_kernel, w.act)
+    out = {
         "workload": w,
         "ms": ms,
         "ms_percentiles": pct,
@@ -169,105 +275,60 @@ def time_workload(name: str, steps: int, warmup: int):
         "tflops": tflops,
         "pct_peak": 100.0 * tflops / peak,
         "ops": ops,
+        "clock": sample_clock(s) if clock else None,
         "roofline": {
             "bound": "mfma",
-            "kernel": kernel_name,
-            "shape": dom[0]["shape"],
-            "achieved": achieved,
+            "kernel": dom_kernel,
+            "launches_per_step": len(dom_tags),
+            "ms_per_launch": round(dom_mean, 5),
+            "achieved": round(achieved, 2),
             "peak": peak,
             "unit": "TFLOP/s",
-            "frac": achieved / peak,
+            "frac": round(achieved / peak, 4),
             "traffic": None if traffic is None else traffic["bytes"],
-            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
-            "algorithmic_bytes": _gemm_bytes(dom[0]["shape"], dom_layout, eb),
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1, calibrated)",
+            "algorithmic_bytes": dom["algorithmic_bytes"],
+            "flops_per_launch": dom["flops"],
             "src": KERNEL_SOURCES[w.act],
         },
         "loss": float(s.loss.item()),
     }
+    if keep_rows:
+        out["gpu_rows"] = _gpu_rows(s, keep_rows)
+    if name in LAUNCH_BOUND:
+        out["launch_modes"] = time_modes(s, steps, warmup)
+    del s
+    torch.cuda.empty_cache()
+    return out
 
 
-# HBM traffic of the dominant kernel, from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE
-# runs summarised under profiles/. A record applies only while the kernel's
-# source file is unchanged (its sha256 is part of the record).
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.md")
-KERNEL_SOURCES = {"bf16": "paper_1603_04467_amd/csrc/gemm_bf16.hip", "f32": "paper_1603_04467_amd/csrc/gemm.hip"}
+def _gpu_rows(s, rows):
+    """Host copies of the step's row-local outputs on batch rows 0..rows-1
+    (the oracle's sample), for the parity ratios."""
+    from paper_1603_04467_amd.step import fused_below
 
-
-def _sha256(path):
-    import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
-
-
-def lookup_traffic(kernel: str, shape, dtype: str):
-    """Bytes per launch (FETCH_SIZE and WRITE_SIZE, each scaled by its
-    calibration factor) recorded for `kernel` at `shape`, or None."""
-    if not os.path.exists(TRAFFIC_FILE):
-        return None
-    src = _sha256(os.path.join(ROOT, KERNEL_SOURCES[dtype]))
-    want = f"{shape[0]}x{shape[1]}x{shape[2]}"
-    for line in open(TRAFFIC_FILE):
-        if not line.startswith("record "):
-            continue
-        kv = dict(item.split("=", 1) for item in line.split()[1:])
-        if kv.get("kernel") == kernel and kv.get("shape") == want and kv.get("src_sha256") == src:
-            fetch = float(kv["fetch_kib"]) * float(kv["fetch_scale"]) * 1024
-            write = float(kv["write_kib"]) * float(kv["write_scale"]) * 1024
-            return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write}
-    return None
-
-
-def cpu_baseline(name: str, rows: int):
-    """Time the oracle's step on the first `rows` batch rows of the workload."""
-    import oracle
-    from paper_1603_04467_amd import workloads
-
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
-    w = workloads.workload(name)
-    inp = workloads.generate(w, seed=0)
-    conv = oracle.bf16_bits_to_f64 if w.act == "bf16" else (lambda a: a.astype(np.float64))
-    x = conv(inp["x"])[:rows]
-    t = None if inp["target"] is None else conv(inp["target"])[:rows]
-    up = None if inp["upstream"] is None else conv(inp["upstream"])[:rows]
-    lab = None if inp.get("labels") is None else inp["labels"][:rows]
-    ws = [conv(a) for a in inp["weights"]]
-    ms_ = None if inp["masters"] is None else [a.astype(np.float64) for a in inp["masters"]]
-    bs = [a.astype(np.float64) for a in inp["biases"]]
-    t0 = time.perf_counter()
-    oracle.dense_step(x, ws, bs, list(w.relus), act=w.act, target=t, upstream_grad=up, lr=w.lr, masters=ms_,
-                      update=w.update, labels=lab)
-    dt = time.perf_counter() - t0
-    flops = w.scaled(batch=rows).flops()
+    def f64(t):
+        return t[:rows].float().cpu().numpy().astype(np.float64)
+    L = s.w.layers
     return {
-        "value": flops / dt / 1e12,
-        "unit": "TFLOP/s",
-        "cores": int(threads),
-        "kind": "oracle",
-        "sample": f"{name}: one full step on batch rows 0..{rows - 1} of {w.batch} "
-                  f"({flops / 1e12:.3f} TFLOP in {dt:.1f} s, float64 numpy)",
+        "h": [f64(t) for t in s.h],
+        "g": f64(s.g),
+        "dy": [f64(s.dy_of(l)) for l in range(L)],
+        "dx": [None if fused_below(s.w, l, s.fuse) else f64(s.dx[l]) for l in range(L)],
     }
 
 
-def time_modes(name: str, steps: int, warmup: int, num_streams: int = 3):
-    """Step time of one workload under four launch modes: one stream in
-    program order ("serial"), independent ops on `num_streams` streams
+def time_modes(s, steps: int, warmup: int, num_streams: int = 3):
+    """Step time under four launch modes, without per-op events: one stream
+    in program order ("serial"), independent ops on `num_streams` streams
     ("streams"), and both captured into a HIP graph and replayed ("graph",
     "graph_streams"). Every step starts from the same Variables (restore
     outside the timed interval); times are HIP-event means in ms."""
     import torch
 
-    from paper_1603_04467_amd import workloads
-    from paper_1603_04467_amd.step import DenseStep
-
-    w = workloads.workload(name)
-    s = DenseStep(w, workloads.generate(w, seed=0))
     stream = torch.cuda.current_stream()
-    graphs = {"graph": s.capture(concurrent=False), "graph_streams": s.capture(concurrent=True,
-                                                                               num_streams=num_streams)}
+    graphs = {"graph": s.capture(concurrent=False),
+              "graph_streams": s.capture(concurrent=True, num_streams=num_streams)}
     modes = {
         "serial": s.run,
         "streams": lambda: s.run_concurrent(num_streams),
@@ -282,7 +343,7 @@ def time_modes(name: str, steps: int, warmup: int, num_streams: int = 3):
         ev = []
         for _ in range(steps):
             s.restore()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a, b = _event(), _event()
             a.record(stream)
             fn()
             b.record(stream)
@@ -290,7 +351,50 @@ def time_modes(name: str, steps: int, warmup: int, num_streams: int = 3):
         torch.cuda.synchronize()
         out[mode] = round(float(np.mean([a.elapsed_time(b) for a, b in ev])), 4)
     best = min(out, key=out.get)
-    return {"ms_per_step": out, "best": best, "tflops_best": round(w.flops() / (out[best] * 1e-3) / 1e12, 3)}
+    return {"ms_per_step": out, "best": best, "tflops_best": round(s.w.flops() / (out[best] * 1e-3) / 1e12, 3)}
+
+
+def time_per_replica(reps: int = 20, replicas: int = 8):
+    """GEMMs of one 4096-wide layer at the per-replica batch of a `replicas`-way
+    data-parallel split (the part of the synchronous data-parallel step one
+    GPU can show): forward, input gradient and weight gradient, fp32 at
+    8192 / replicas rows and 16-bit at 16384 / replicas rows."""
+    import torch
+
+    from paper_1603_04467_amd import tfdense as T
+
+    stream = torch.cuda.current_stream()
+    out = {}
+    for dt, batch in (("f32", 8192), ("bf16", 16384)):
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        n = batch // replicas
+        x = torch.randn(n, 4096, device="cuda").to(tdt)
+        wt = (torch.randn(4096, 4096, device="cuda") / 64).to(tdt)
+        dy = torch.randn(n, 4096, device="cuda").to(tdt)
+        bias = torch.zeros(4096, device="cuda")
+        y = torch.empty(n, 4096, dtype=tdt, device="cuda")
+        dw = torch.empty(4096, 4096, device="cuda")
+        calls = {
+            f"fwd {n}x4096x4096 NT": lambda: T.tfd_matmul(x, wt, y, transpose_b=True, bias=bias, epilogue="bias_relu"),
+            f"dx {n}x4096x4096 NT": lambda: T.tfd_matmul(dy, wt, y, transpose_b=True),
+            f"dw 4096x4096x{n} TN": lambda: T.tfd_matmul(x, dy, dw, transpose_a=True),
+        }
+        res = {}
+        for name, fn in calls.items():
+            for _ in range(3):
+                fn()
+            ev = [_event() for _ in range(reps + 1)]
+            ev[0].record(stream)
+            for i in range(reps):
+                fn()
+                ev[i + 1].record(stream)
+            torch.cuda.synchronize()
+            ms = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
+            f = 2 * n * 4096 * 4096
+            res[name] = {"ms": round(ms, 4), "tflops": round(f / (ms * 1e-3) / 1e12, 1),
+                         "frac": round(f / (ms * 1e-3) / 1e12 / PEAK_TFLOPS[dt], 3)}
+        out[f"{dt} batch {batch}/{replicas}"] = res
+    return out
 
 
 def time_conversions(count: int = 1 << 26, reps: int = 20):
@@ -314,7 +418,7 @@ def time_conversions(count: int = 1 << 26, reps: int = 20):
     for name, (fn, byt) in calls.items():
         for _ in range(3):
             fn()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev = [_event() for _ in range(reps + 1)]
         ev[0].record(stream)
         for i in range(reps):
             fn()
@@ -326,17 +430,219 @@ def time_conversions(count: int = 1 << 26, reps: int = 20):
     return out
 
 
+# ----------------------------------------------------------------- records
+
+def _sha256(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def lookup_traffic(kernel: str, dtype: str):
+    """Bytes per launch (FETCH_SIZE and WRITE_SIZE, each scaled by its
+    calibration factor) recorded for `kernel` in profiles/traffic.md, or None.
+    A record applies only while the kernel's source file is unchanged (its
+    sha256 is part of the record)."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    src = _sha256(os.path.join(ROOT, KERNEL_SOURCES[dtype]))
+    for line in open(TRAFFIC_FILE):
+        if not line.startswith("record "):
+            continue
+        kv = dict(item.split("=", 1) for item in line[len("record "):].strip().split(" ; "))
+        if kv.get("kernel") == kernel and kv.get("src_sha256") == src:
+            fetch = float(kv["fetch_kib"]) * float(kv["fetch_scale"]) * 1024
+            write = float(kv["write_kib"]) * float(kv["write_scale"]) * 1024
+            return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write}
+    return None
+
+
+def revision():
+    """git revision of the tree when .git is present, and a hash of the
+    library sources either way."""
+    rev = None
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short=12", "HEAD"], capture_output=True, text=True,
+                           timeout=10)
+        if r.returncode == 0:
+            rev = r.stdout.strip()
+    except (OSError, subprocess.TimeoutExpired):
+        pass
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1603_04467_amd", "csrc", "*"))):
+        h.update(os.path.basename(p).encode())
+        h.update(open(p, "rb").read())
+    return {"git": rev, "csrc_sha256": h.hexdigest()[:16]}
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+# ----------------------------------------------------------------- oracle leg
+
+def _oracle_inputs(w, rows):
+    import oracle
+    from paper_1603_04467_amd import workloads
+
+    inp = workloads.generate(w, seed=0)
+    conv = oracle.bf16_bits_to_f64 if w.act == "bf16" else (lambda a: a.astype(np.float64))
+    sl = slice(0, rows)
+    return {
+        "x": conv(inp["x"])[sl],
+        "weights": [conv(a) for a in inp["weights"]],
+        "biases": [a.astype(np.float64) for a in inp["biases"]],
+        "masters": None if inp["masters"] is None else [a.astype(np.float64) for a in inp["masters"]],
+        "target": None if inp["target"] is None else conv(inp["target"])[sl],
+        "upstream": None if inp["upstream"] is None else conv(inp["upstream"])[sl],
+        "labels": None if inp.get("labels") is None else inp["labels"][sl],
+    }
+
+
+def _run_oracle(w, hi):
+    import oracle
+    return oracle.dense_step(hi["x"], hi["weights"], hi["biases"], list(w.relus), act=w.act, target=hi["target"],
+                             upstream_grad=hi["upstream"], lr=w.lr, masters=hi["masters"], update=w.update,
+                             labels=hi["labels"], rounding=w.rounding)
+
+
+def _parity(w, hi, ref, gpu, tau):
+    """Normalised errors max|err| / D of the GPU's row-local outputs against
+    the oracle's chain on the same rows (D as in the parity tests), and the
+    ReLU decisions: how many differ from the sign of the oracle's
+    pre-activation, all of which must lie in the band |y| <= tau D."""
+    import oracle
+
+    def ne(got, want, D):
+        return float(np.max(np.abs(got - want)) / D) if got.size and D > 0 else 0.0
+
+    out, flips, band = {}, 0, 0
+    amax = lambda a: float(np.max(np.abs(a))) if np.size(a) else 0.0  # noqa: E731
+    D_fwd = []
+    for l in range(w.layers):
+        D = w.dims[l] * amax(ref["h"][l]) * amax(hi["weights"][l]) + amax(hi["biases"][l])
+        D_fwd.append(D)
+        out[f"H{l + 1}"] = ne(gpu["h"][l + 1], ref["h"][l + 1], D)
+        if w.relus[l]:
+            y = oracle.matmul(ref["h"][l], hi["weights"][l], out="f64", bias=hi["biases"][l])
+            inb = np.abs(y) <= tau * D
+            diff = (gpu["h"][l + 1] > 0) != (y > 0)
+            band += int(inb.sum())
+            flips += int(diff.sum())
+            out[f"relu{l + 1}_flips_outside_band"] = int((diff & ~inb).sum())
+    D_g = D_fwd[-1] + amax(ref["g"]) if w.cost != "upstream" else amax(ref["g"])
+    out["G"] = ne(gpu["g"], ref["g"], D_g)
+    # row-local gradients on rows no ReLU flip touched
+    touched = np.zeros(gpu["g"].shape[0], dtype=bool)
+    for l in range(w.layers):
+        if w.relus[l]:
+            touched |= np.any((gpu["h"][l + 1] > 0) != (ref["h"][l + 1] > 0), axis=1)
+    keep = ~touched
+    for l in reversed(range(w.layers)):
+        md = amax(ref["dy"][l])
+        out[f"dY{l + 1}"] = ne(gpu["dy"][l][keep], ref["dy"][l][keep], D_g)
+        D_g = w.dims[l + 1] * md * amax(hi["weights"][l])
+        if gpu["dx"][l] is not None:
+            out[f"dX{l + 1}"] = ne(gpu["dx"][l][keep], ref["dx"][l][keep], D_g)
+    return {"max_err_over_D": {k: (round(v, 8) if isinstance(v, float) else v) for k, v in out.items()},
+            "relu_flips": flips, "mask_band_count": band, "rows_compared": int(keep.sum()), "tau": tau}
+
+
+def cpu_baseline(results, threads):
+    """The oracle's full step on bounded row samples of every workload, on
+    the host cores; C1 and C2 whole (median of 5, and with one thread).
+    Returns the headline workload's figure with the others beside it."""
+    from threadpoolctl import threadpool_limits
+
+    from paper_1603_04467_amd import workloads
+
+    tau = {"f32": 1e-5, "bf16": 1e-2}
+    per = {}
+    for name, rows in CPU_ROWS.items():
+        w = workloads.workload(name)
+        rows = rows or w.batch
+        hi = _oracle_inputs(w, rows)
+        reps = 5 if rows == w.batch else 1
+        times = []
+        with threadpool_limits(limits=threads):
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                ref = _run_oracle(w, hi)
+                times.append(time.perf_counter() - t0)
+        dt = float(np.median(times))
+        flops = w.scaled(batch=rows).flops()
+        d = {"rows": rows, "of_batch": w.batch, "step_s": round(dt, 4), "tflops": round(flops / dt / 1e12, 5),
+             "repeats": reps}
+        if rows == w.batch:
+            t1 = []
+            with threadpool_limits(limits=1):
+                for _ in range(reps):
+                    t0 = time.perf_counter()
+                    _run_oracle(w, hi)
+                    t1.append(time.perf_counter() - t0)
+            d["step_s_one_thread"] = round(float(np.median(t1)), 4)
+        r = results.get(name)
+        if r is not None and r.get("gpu_rows") is not None:
+            g = {k: v for k, v in r["gpu_rows"].items()}
+            g = {"h": [a[:rows] for a in g["h"]], "g": g["g"][:rows], "dy": [a[:rows] for a in g["dy"]],
+                 "dx": [None if a is None else a[:rows] for a in g["dx"]]}
+            d["parity"] = _parity(w, hi, ref, g, tau[w.act])
+        per[name] = d
+    head = per[PRIMARY]
+    return {
+        "value": head["tflops"],
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{PRIMARY}: one full step (forward, gradients, update) on batch rows 0..{head['rows'] - 1} of "
+                  f"{head['of_batch']}, float64 numpy, in {head['step_s']} s",
+        "cpu_model": cpu_model(),
+        "workloads": per,
+    }
+
+
+# ----------------------------------------------------------------- main
+
 def _per_op(ops):
-    """Mean ms per op, with TFLOP/s (GEMMs) or GB/s (memory-bound ops)."""
     out = {}
     for k, v in ops.items():
         d = {"ms": round(v["ms"], 4)}
         if "tflops" in v:
             d["tflops"] = round(v["tflops"], 1)
+            d["kernel"] = v["kernel"]
         if "gbs" in v:
             d["gbs"] = round(v["gbs"], 1)
         out[k] = d
     return out
+
+
+def _entry(name, r):
+    e = {
+        "workload": name,
+        "value": round(r["tflops"], 3),
+        "unit": "TFLOP/s",
+        "ms_per_step": round(r["ms"], 4),
+        "ms_per_step_percentiles": r["ms_percentiles"],
+        "pct_mfma_peak": round(r["pct_peak"], 2),
+        "roofline": r["roofline"],
+        "per_op": _per_op(r["ops"]),
+        "loss": r["loss"],
+    }
+    if "launch_modes" in r:
+        lm = r["launch_modes"]
+        best = lm["ms_per_step"][lm["best"]]
+        e["launch_modes"] = lm
+        e["ms_per_step_marked"] = e["ms_per_step"]
+        e["ms_per_step"] = best
+        e["value"] = round(r["workload"].flops() / (best * 1e-3) / 1e12, 3)
+        e["pct_mfma_peak"] = round(100 * e["value"] / PEAK_TFLOPS[r["workload"].act], 3)
+        e["value_source"] = f"fastest unmarked launch mode ({lm['best']})"
+    return e
 
 
 def main():
@@ -347,7 +653,6 @@ def main():
     ap.add_argument("--workload", default=PRIMARY)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=16384)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -358,9 +663,13 @@ def main():
     import torch
     assert torch.cuda.is_available(), "no GPU visible"
     torch.cuda.set_device(0)
+    want_rows = not args.no_cpu_baseline
 
     print(f"bench: timing {args.workload} ({args.steps} steps, {args.warmup} warm-up)", file=sys.stderr, flush=True)
-    r = time_workload(args.workload, args.steps, args.warmup)
+    results = {}
+    keep = (CPU_ROWS.get(args.workload) or workloads_batch(args.workload)) if want_rows else 0
+    r = time_workload(args.workload, args.steps, args.warmup, keep_rows=keep, clock=True)
+    results[args.workload] = r
     w = r["workload"]
     out = {
         "metric": METRIC,
@@ -391,33 +700,32 @@ def main():
         "pct_mfma_peak": round(r["pct_peak"], 2),
         "roofline": r["roofline"],
         "per_op": _per_op(r["ops"]),
+        "sclk_mhz": r["clock"],
         "loss": r["loss"],
+        "revision": revision(),
     }
     if not args.no_secondary and args.workload == PRIMARY:
         out["also"] = []
         for name in SECONDARY:
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
-            r2 = time_workload(name, args.steps, args.warmup)
-            out["also"].append({
-                "workload": name,
-                "value": round(r2["tflops"], 3),
-                "unit": "TFLOP/s",
-                "ms_per_step": round(r2["ms"], 4),
-                "ms_per_step_percentiles": r2["ms_percentiles"],
-                "pct_mfma_peak": round(r2["pct_peak"], 2),
-                "roofline": r2["roofline"],
-                "per_op": _per_op(r2["ops"]),
-                "loss": r2["loss"],
-            })
-            if name in LAUNCH_BOUND:
-                out["also"][-1]["launch_modes"] = time_modes(name, args.steps, args.warmup)
-    if not args.no_secondary and args.workload == PRIMARY:
+            keep = (CPU_ROWS.get(name) or workloads_batch(name)) if (want_rows and name in CPU_ROWS) else 0
+            r2 = time_workload(name, args.steps, args.warmup, keep_rows=keep)
+            results[name] = r2
+            out["also"].append(_entry(name, r2))
+        print("bench: timing the per-replica GEMM shapes", file=sys.stderr, flush=True)
+        out["per_replica"] = time_per_replica()
         print("bench: timing the 32 <-> 16-bit conversions", file=sys.stderr, flush=True)
         out["conversions"] = time_conversions()
-    if not args.no_cpu_baseline:
-        print(f"bench: timing the oracle on {args.cpu_rows} rows", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_rows)
+    if want_rows:
+        threads = len(os.sched_getaffinity(0))
+        print(f"bench: timing the oracle on {threads} host threads", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(results, threads)
     print(json.dumps(out), flush=True)
+
+
+def workloads_batch(name):
+    from paper_1603_04467_amd import workloads
+    return workloads.workload(name).batch
 
 
 if __name__ == "__main__":

@@ -410,6 +410,20 @@ TFD_API tfd_status tfd_convert_f32_to_bf16(const float* src, uint16_t* dst, int6
                                    tfd_rounding rounding, void* stream);
 TFD_API tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int64_t count, void* stream);
 
+/*
+ * Engine clock probe (measurement support for benchmarks; not an op of the
+ * training step). One wave of 64 lanes runs `iterations` dependent fp32 FMAs
+ * between two reads of the shader clock counter and of the constant 100 MHz
+ * real-time counter, and writes counters[0] = shader clock cycles elapsed,
+ * counters[1] = real-time ticks elapsed, counters[2] = the FMA chain's result
+ * (it keeps the chain from being removed). The clock of the compute unit the
+ * wave ran on, in MHz, is 100 * counters[0] / counters[1]; launched on a
+ * second stream while other work runs, it measures the clock under that load.
+ * counters: device, 3 uint64 (written, not read). iterations in [1, 2^31),
+ * else TFD_EINVAL.
+ */
+TFD_API tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

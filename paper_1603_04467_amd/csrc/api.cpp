@@ -850,4 +850,12 @@ tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int64_t coun
   return hip_status(tfd::launch_convert_to_f32(src, dst, count, as_stream(stream)), "tfd_convert_bf16_to_f32 launch");
 }
 
+tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void* stream) {
+  g_err[0] = 0;
+  if (!counters) return fail(TFD_EINVAL, "tfd_clock_probe: NULL counters");
+  if (iterations < 1 || iterations >= (int64_t(1) << 31))
+    return fail(TFD_EINVAL, "tfd_clock_probe: iterations %lld outside [1, 2^31)", (long long)iterations);
+  return hip_status(tfd::launch_clock_probe(counters, iterations, as_stream(stream)), "tfd_clock_probe launch");
+}
+
 }  // extern "C"

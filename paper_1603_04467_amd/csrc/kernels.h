@@ -89,6 +89,9 @@ hipError_t launch_relu_grad_bias_add_grad(const void* g, const void* f, void* ou
 // once per device).
 size_t static_scratch_bytes();
 hipError_t static_scratch(void** out);
+// Engine clock probe: counters[0] = shader clock cycles, counters[1] = 100 MHz
+// real-time ticks over the same run of `iterations` dependent FMAs.
+hipError_t launch_clock_probe(uint64_t* counters, int64_t iterations, hipStream_t s);
 // The same with the Relu test read from a bit mask (rows x ldm words).
 hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,
                                                float* db, int64_t rows, int64_t cols, bool bf16, void* ws,

@@ -37,7 +37,7 @@ EXPORTS = (
     "tfd_apply_gradient_descent_matrix", "tfd_convert_f32_to_bf16", "tfd_convert_bf16_to_f32",
     "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
     "tfd_matmul_relu_mask_grad_bias_add_grad", "tfd_matmul_workspace_size", "tfd_matmul_with_workspace",
-    "tfd_set_tuning", "tfd_relu_grad_bias_add_grad_noalloc",
+    "tfd_set_tuning", "tfd_relu_grad_bias_add_grad_noalloc", "tfd_clock_probe",
 )
 
 
@@ -100,6 +100,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
                                                      vp, sz, vp], i32),
         "tfd_set_tuning": ([ctypes.c_char_p, i32], i32),
         "tfd_relu_grad_bias_add_grad_noalloc": ([vp, vp, vp, vp, i64, i64, i32, vp], i32),
+        "tfd_clock_probe": ([vp, i64, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -514,3 +515,12 @@ def tfd_convert_bf16_to_f32(src, dst, stream=None):
         raise ValueError("src must be bfloat16 and dst contiguous fp32 of the same size")
     _check(load().tfd_convert_bf16_to_f32(_ptr(src), _ptr(dst), n, _stream(stream)))
     return dst
+
+
+def tfd_clock_probe(counters, iterations, stream=None):
+    """One wave's shader clock cycles and 100 MHz real-time ticks over
+    `iterations` dependent FMAs into counters (int64 device tensor of 3)."""
+    if counters.dtype != torch.int64 or counters.numel() != 3 or not counters.is_contiguous():
+        raise ValueError("counters must be a contiguous int64 tensor of 3 elements")
+    _check(load().tfd_clock_probe(_ptr(counters), int(iterations), _stream(stream)))
+    return counters

@@ -140,6 +140,12 @@ def test_softmax_and_conversion_validation(lib):
     assert lib.tfd_apply_gradient_descent_matrix(FAKE, ctypes.c_float(0.01), FAKE * 2, 10, 10, None, None, 5,
                                                  None) == 1
 
+    # clock probe: counters required, iterations in [1, 2^31)
+    assert lib.tfd_clock_probe(None, 100, None) == 1
+    assert lib.tfd_clock_probe(FAKE, 0, None) == 1
+    assert lib.tfd_clock_probe(FAKE, 1 << 31, None) == 1
+    assert b"iterations" in lib.tfd_last_error()
+
 
 def test_fused_relu_grad_matmul_validation(lib):
     f = lib.tfd_matmul_relu_grad_bias_add_grad
