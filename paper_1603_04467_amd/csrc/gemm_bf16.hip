@@ -934,18 +934,15 @@ bool gemm_bf16_256_ok(const GemmDesc& d) {
 
 hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // A is k-contiguous unless transposed; B is k-contiguous when transposed.
-  // Defaults measured on the step's shapes: 8 waves (2 per SIMD) for NN, 16
-  // for TN, whose two transposing-read operands gain most from more waves to
-  // hide LDS latency; for NT the scheduled 4-wave loop over a long k range
-  // (forward and input-gradient products of the 4096-wide layers), except
-  // under the ReluGrad epilogues, whose feature or mask reads cost the 4-wave
-  // epilogue more than its loop saves; 8 waves otherwise.
+  // Defaults measured inside the training step: 8 waves (2 per SIMD) for
+  // NN and NT, 16 waves for TN, whose two transposing-read operands gain most
+  // from more waves to hide LDS latency. The scheduled 4-wave NT loop (the
+  // tuning knob's 4) runs a k loop of its own about 10% faster on random
+  // operands, but its epilogue over 256 accumulators per lane spills, and
+  // within the step, on ReLU-sparse operands, its forward products take
+  // 5-10% longer than with 8 waves.
   if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, 8), s);
-  if (!d.ta && d.tb) {
-    const bool long_k = d.k >= 2048 && d.splits <= 1;
-    const bool relu_grad = d.mask_in != nullptr || d.features != nullptr;
-    return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, long_k && !relu_grad ? 4 : 8), s);
-  }
+  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, 8), s);
   return launch_gemm_bf16_256_tn(d, s);
 }
 #endif
