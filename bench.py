@@ -110,9 +110,15 @@ def op_info(s, tag):
             m, n, k, lay = w.dims[l], w.dims[l + 1], N, "TN"
             epi = "none"
         out = "f32" if kind == "dw" else w.act
+        ob = 4 if out == "f32" else eb
+        # operands in, product out, plus what the fused epilogue reads and writes
+        extra = {"bias_relu+mask": m * n // 8 + 4 * n, "bias_relu": 4 * n, "bias": 4 * n,
+                 "bias+sq_err+colsum": 2 * m * n * eb + 4 * n + 4 * n * (m // 256),
+                 "relugrad_mask+colsum": m * n // 8 + 4 * n * (m // 256),
+                 "relugrad+colsum": m * n * eb + 4 * n * (m // 256)}.get(epi, 0)
         d.update(layout=lay, epi=epi, shape=[m, n, k], flops=2 * m * n * k,
                  kernel=f"gemm {w.act} {lay} {epi} {m}x{n}x{k} -> {out}",
-                 algorithmic_bytes=m * k * eb + k * n * eb + m * n * (4 if out == "f32" else eb))
+                 algorithmic_bytes=m * k * eb + k * n * eb + m * n * ob + extra)
     elif kind == "relugrad":
         M = w.dims[l + 1]
         if not w.relus[l]:
@@ -137,39 +143,38 @@ def _clock_probe_mhz(counters):
     return [100.0 * float(r[0]) / float(r[1]) for r in c if r[1] > 0]
 
 
-def sample_clock(s, probes: int = 8, iterations: int = 500_000):
+def sample_clock(s, probes: int = 8, iterations: int = 50_000):
     """Engine clock in MHz, from tfd_clock_probe (shader clock cycles over
-    100 MHz real-time ticks in one wave): `probes` probes on a second stream
-    while step `s` runs back to back on the launch stream (restored Variables,
-    as in the timed pass), and as many with the GPU otherwise idle."""
+    100 MHz real-time ticks in one wave, about 1 ms): `probes` probes each
+    enqueued right behind a step (restored Variables, as in the timed pass),
+    so that it runs at the clock the step left the GPU at, and as many with
+    the GPU idle before. The probe runs on the launch stream, never beside a
+    step: a wave of its own on one compute unit would keep a workgroup of the
+    whole-tile GEMMs (one per compute unit, one round over the chip) off that
+    unit and stretch the GEMM it overlaps."""
     import torch
 
     from paper_1603_04467_amd import tfdense as T
 
-    side = torch.cuda.Stream()
-    loaded = torch.zeros(probes, 3, dtype=torch.int64, device="cuda")
+    after = torch.zeros(probes, 3, dtype=torch.int64, device="cuda")
     idle = torch.zeros(probes, 3, dtype=torch.int64, device="cuda")
-    for i in range(probes):
-        T.tfd_clock_probe(idle[i], iterations)
     torch.cuda.synchronize()
     for i in range(probes):
+        T.tfd_clock_probe(idle[i], iterations)
+        torch.cuda.synchronize()
+        time.sleep(0.01)
+    for i in range(probes):
         s.restore()
         s.run()
-        side.wait_stream(torch.cuda.current_stream())
-        s.restore()
-        s.run()
-        with torch.cuda.stream(side):
-            T.tfd_clock_probe(loaded[i], iterations)
-        s.restore()
-        s.run()
+        T.tfd_clock_probe(after[i], iterations)
     torch.cuda.synchronize()
 
     def stats(v):
         return {"median": round(float(np.median(v)), 1), "min": round(float(np.min(v)), 1),
                 "max": round(float(np.max(v)), 1), "probes": len(v)} if v else None
-    return {"under_load": stats(_clock_probe_mhz(loaded)), "idle": stats(_clock_probe_mhz(idle)),
-            "source": "tfd_clock_probe: 100 * s_memtime cycles / s_memrealtime ticks of one wave; under_load "
-                      "on a second stream while the step runs"}
+    return {"after_step": stats(_clock_probe_mhz(after)), "idle": stats(_clock_probe_mhz(idle)),
+            "source": "tfd_clock_probe: 100 * s_memtime cycles / s_memrealtime ticks of one wave over about 1 ms; "
+                      "after_step: enqueued right behind a step on the launch stream"}
 
 
 # ----------------------------------------------------------------- timing
@@ -615,6 +620,7 @@ def _per_op(ops):
         if "tflops" in v:
             d["tflops"] = round(v["tflops"], 1)
             d["kernel"] = v["kernel"]
+            d["algorithmic_bytes"] = v["algorithmic_bytes"]
         if "gbs" in v:
             d["gbs"] = round(v["gbs"], 1)
         out[k] = d

@@ -1,0 +1,98 @@
+"""The rocprofv3 summariser (paper_1603_04467_amd/profiling.py) on small
+synthetic outputs: kernel ids map to the compiled symbols, the roofline
+check reproduces a known fraction, traffic records scale by the copy
+calibration and round-trip through bench.py's lookup."""
+
+import csv
+import json
+import os
+import re
+
+import pytest
+
+from paper_1603_04467_amd import profiling as P
+
+TN = "_ZN3tfd12_GLOBAL__N_113gemm_bf16_256ILb0ELb0EfLi4ELi4ELi0EEEvNS0_6ParamsE"
+NT_MASK = "_ZN3tfd12_GLOBAL__N_113gemm_bf16_256ILb1ELb1EDF16bLi2ELi4ELi4EEEvNS0_6ParamsE"
+NT_PLAIN = "_ZN3tfd12_GLOBAL__N_113gemm_bf16_256ILb1ELb1EDF16bLi2ELi4ELi0EEEvNS0_6ParamsE"
+COPY = "__amd_rocclr_copyBuffer"
+TN_ID = "gemm bf16 TN none 4096x4096x16384 -> f32"
+NT_ID = "gemm bf16 NT bias_relu+mask 16384x4096x4096 -> bf16"
+
+
+def test_kernel_ids_and_symbols():
+    kid = P.parse_kernel_id(TN_ID)
+    assert (kid["layout"], kid["out"], kid["m"], kid["k"]) == ("TN", "f32", 4096, 16384)
+    assert P.matches(kid, TN, 256 * 1024)
+    assert not P.matches(kid, TN, 512 * 1024)           # other grid: another shape
+    assert not P.matches(kid, NT_PLAIN, 256 * 1024)
+    nt = P.parse_kernel_id(NT_ID)
+    assert P.matches(nt, NT_MASK, 1024 * 512)
+    assert not P.matches(nt, NT_PLAIN, 1024 * 512)      # epilogue differs
+    assert P.symbol_fields("void tfd::(anonymous namespace)::gemm_bf16_256<true, true, __bf16, 2, 4, 4>(Params)") == \
+        {"a_kc": True, "b_kc": True, "out": "bf16", "waves": (2, 4), "ep": 4}
+    with pytest.raises(ValueError):
+        P.parse_kernel_id("sgd")
+
+
+def _write(path, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=list(rows[0]))
+        w.writeheader()
+        w.writerows(rows)
+
+
+def _bench(path, frac=0.5):
+    peak = 2516.6
+    flops = 2 * 4096 * 4096 * 16384
+    ms = flops / (frac * peak * 1e12) * 1e3
+    line = {"steps": 20, "roofline": {"kernel": TN_ID, "launches_per_step": 4, "ms_per_launch": ms,
+                                      "achieved": frac * peak, "peak": peak, "frac": frac, "flops_per_launch": flops},
+            "per_op": {"dw1": {"ms": ms, "kernel": TN_ID}, "fwd1": {"ms": 0.5, "kernel": NT_ID}, "sgd1": {"ms": 0.05}}}
+    with open(path, "w") as f:
+        f.write("noise\n" + json.dumps(line) + "\n")
+    return ms
+
+
+def test_trace_reproduces_the_fraction(tmp_path):
+    ms = _bench(tmp_path / "b.json", frac=0.5)
+    ns = int(ms * 1e6)
+    trace = [{"Kernel_Name": TN, "Grid_Size_X": 256 * 1024, "Start_Timestamp": 1000 * i, "End_Timestamp": 1000 * i + ns}
+             for i in range(8)]
+    trace.append({"Kernel_Name": NT_MASK, "Grid_Size_X": 1024 * 512, "Start_Timestamp": 0, "End_Timestamp": 5})
+    _write(tmp_path / "run_kernel_trace.csv", trace)
+    _write(tmp_path / "run_kernel_stats.csv", [
+        {"Name": TN, "Calls": 8, "TotalDurationNs": 8 * ns, "AverageNs": ns, "Percentage": 99.0, "MinNs": ns,
+         "MaxNs": ns}])
+    text = P.trace(str(tmp_path), str(tmp_path / "b.json"))
+    assert "| rocprofv3 kernel trace (every launch in the run) | 8 |" in text
+    assert "0.5000 |" in text and re.search(r"difference of the fractions: [+-]0\.00%", text)
+
+
+def test_traffic_records_round_trip(tmp_path, monkeypatch):
+    _bench(tmp_path / "b.json")
+    os.makedirs(tmp_path / "f")
+    os.makedirs(tmp_path / "w")
+    # the counters read half the bytes of a copy for FETCH_SIZE, all of them for WRITE_SIZE
+    base = {"Grid_Size_X": 256 * 1024}
+    _write(tmp_path / "f" / "run_counter_collection.csv", [
+        dict(base, Kernel_Name=COPY, Counter_Name="FETCH_SIZE", Counter_Value=32768.0),
+        dict(base, Kernel_Name=COPY, Counter_Name="FETCH_SIZE", Counter_Value=100.0),
+        dict(base, Kernel_Name=TN, Counter_Name="FETCH_SIZE", Counter_Value=400000.0),
+        dict(base, Kernel_Name=TN, Counter_Name="FETCH_SIZE", Counter_Value=402000.0)])
+    _write(tmp_path / "w" / "run_counter_collection.csv", [
+        dict(base, Kernel_Name=COPY, Counter_Name="WRITE_SIZE", Counter_Value=65536.0),
+        dict(base, Kernel_Name=TN, Counter_Name="WRITE_SIZE", Counter_Value=65600.0),
+        dict(base, Kernel_Name=TN, Counter_Name="WRITE_SIZE", Counter_Value=65600.0)])
+    text = P.traffic(str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "b.json"))
+    assert "x 2.0000" in text and "x 1.0000" in text
+    rec = [ln for ln in text.splitlines() if ln.startswith("record ")]
+    assert len(rec) == 1 and f"kernel={TN_ID} ;" in rec[0]
+    # bench.py reads the record back while the kernel source is unchanged
+    import bench
+    tf = tmp_path / "traffic.md"
+    tf.write_text("\n".join(rec) + "\n")
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tf))
+    got = bench.lookup_traffic(TN_ID, "bf16")
+    want = 401000.0 * 1024 * 2.0 + 65600.0 * 1024 * 1.0
+    assert got is not None and abs(got["bytes"] - want) <= 1e-6 * want
