@@ -424,6 +424,84 @@ TFD_API tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int6
  */
 TFD_API tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void* stream);
 
+/*
+ * One whole training step of a small fp32 multilayer perceptron in a single
+ * persistent kernel: the forward pass H_l = Relu(H_{l-1} W_l + b_l) (Figure 1;
+ * MatMul, Add and ReLU of section 2, Table 1), the cost head, the gradient
+ * subgraph that automatic differentiation adds (section 4.1: ReluGrad, the
+ * transposed MatMuls, BiasAddGrad) and the SGD update of the Variables (the
+ * in-place update of section 2, "Variables"). The same computation as the
+ * per-op calls above, for steps too small to fill the GPU one kernel at a time
+ * (a few hundred rows, layers of a few thousand units), where launch gaps
+ * dominate: the ops run as phases separated by grid-wide barriers in one
+ * cooperative launch, each phase's MatMul tiles, column sums and update chunks
+ * spread over the workgroups.
+ *
+ * Layer l (0-based, up to TFD_MLP_MAX_LAYERS), all fp32 row-major with
+ * leading dimension = row length:
+ *   weights [fan_in, fan_out] W_l (read, then updated in place when `update`),
+ *   bias [fan_out] b_l (likewise), activations [batch, fan_out] H_{l+1}
+ *   (written), backprop [batch, fan_out] dY_l (written; required for a Relu
+ *   layer, ignored otherwise), weight_grad [fan_in, fan_out] dW_l and
+ *   bias_grad [fan_out] db_l (written). fan_in of layer l must equal fan_out of
+ *   layer l - 1; every layer but the last must have a Relu (relu != 0).
+ * x [batch, fan_in of layer 0] is the input; input_grad [batch, same] receives
+ * dX_0 = dY_0 W_0^T when not NULL. cost: TFD_COST_SQUARED_ERROR,
+ * L = 1/2 sum (out - target)^2 (target NULL: target 0), G = out - target; or
+ * TFD_COST_SOFTMAX_XENT with int32 labels [batch], L = sum_n (log sum_j
+ * exp(z_nj) - z_n,y_n), G = softmax(z) - onehot(y) (a label outside
+ * [0, classes) gives a NaN loss). cost_grad [batch, classes] receives G and
+ * *loss (device float64) L. The output layer's dY is ReluGrad(G, out) when it
+ * has a Relu, else G itself (its backprop is not written). Every Variable is
+ * updated as var - learning_rate * grad, rounded once.
+ *
+ * workspace: tfd_mlp_step_workspace_size(desc) bytes, 8-byte aligned. Its
+ * first 4096 bytes hold the grid barrier (an error word at offset 0, a
+ * generation count at 256, arrival counters from 512 on) and must be zero
+ * before the first call on it; a call that completes normally leaves the
+ * error word and the arrival counters at zero (the generation count
+ * advances), ready for the next. If a barrier wait times out (only possible
+ * if the grid were not all resident), the error word is nonzero once the
+ * stream has reached the call, the outputs are incomplete, and the first 4096
+ * bytes must be zeroed again before the workspace is reused. Calls that share a workspace must not
+ * overlap. Results are bitwise reproducible. Buffers must not overlap each
+ * other except as stated. Errors: TFD_EINVAL for NULL required pointers,
+ * sizes out of range (layers in [1, TFD_MLP_MAX_LAYERS], batch and fans in
+ * [1, 2^20], batch x fan and fan_in x fan_out below 2^31), mismatched fans, a
+ * small or misaligned workspace; TFD_EUNSUPPORTED for a hidden layer without
+ * a Relu; TFD_EHIP if the cooperative launch is refused. batch == 0 enqueues
+ * nothing.
+ */
+#define TFD_MLP_MAX_LAYERS 4
+typedef enum tfd_cost { TFD_COST_SQUARED_ERROR = 0, TFD_COST_SOFTMAX_XENT = 1 } tfd_cost;
+typedef struct tfd_mlp_layer {
+  float* weights;
+  float* bias;
+  float* activations;
+  float* backprop;
+  float* weight_grad;
+  float* bias_grad;
+  int64_t fan_in, fan_out;
+  int32_t relu;
+} tfd_mlp_layer;
+typedef struct tfd_mlp_step_desc {
+  int32_t layers;
+  int64_t batch;
+  const float* x;
+  float* input_grad;
+  tfd_mlp_layer layer[TFD_MLP_MAX_LAYERS];
+  int32_t cost;
+  const float* target;
+  const int32_t* labels;
+  float* cost_grad;
+  double* loss;
+  float learning_rate;
+  int32_t update;
+} tfd_mlp_step_desc;
+TFD_API size_t tfd_mlp_step_workspace_size(const tfd_mlp_step_desc* desc);
+TFD_API tfd_status tfd_mlp_step(const tfd_mlp_step_desc* desc, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
 #ifdef __cplusplus
 }
 #endif

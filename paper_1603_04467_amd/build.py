@@ -19,7 +19,7 @@ OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtfdense.so")
 
 SOURCES = ["gemm.hip", "gemm_bf16.hip", "gemm_bf16_tn.hip", "gemm_small.hip", "elementwise.hip", "reduce.hip",
-           "softmax.hip", "convert.hip", "diag.hip", "api.cpp"]
+           "softmax.hip", "convert.hip", "diag.hip", "step_fused.hip", "api.cpp"]
 # Per-source compiler flags: the TN whole-tile GEMM takes the max-ILP machine
 # scheduler (measured 2 % faster for it, slower for the other layouts).
 SOURCE_FLAGS = {"gemm_bf16_tn.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]}

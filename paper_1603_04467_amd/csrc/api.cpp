@@ -859,3 +859,84 @@ tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void* stream)
 }
 
 }  // extern "C"
+
+namespace {
+
+// Checks a step descriptor; fills `out` when valid.
+tfd_status mlp_check(const tfd_mlp_step_desc* d, const char* fn, tfd::MlpStep* out) {
+  if (!d) return fail(TFD_EINVAL, "%s: NULL descriptor", fn);
+  const int L = d->layers;
+  if (L < 1 || L > TFD_MLP_MAX_LAYERS) return fail(TFD_EINVAL, "%s: layers %d outside [1, %d]", fn, L, TFD_MLP_MAX_LAYERS);
+  const int64_t lim = int64_t(1) << 20, big = int64_t(1) << 31;
+  if (d->batch < 0 || d->batch > lim) return fail(TFD_EINVAL, "%s: batch %lld outside [0, 2^20]", fn, (long long)d->batch);
+  if (d->cost != TFD_COST_SQUARED_ERROR && d->cost != TFD_COST_SOFTMAX_XENT)
+    return fail(TFD_EINVAL, "%s: unknown cost %d", fn, d->cost);
+  for (int l = 0; l < L; ++l) {
+    const tfd_mlp_layer& y = d->layer[l];
+    if (y.fan_in < 1 || y.fan_in > lim || y.fan_out < 1 || y.fan_out > lim)
+      return fail(TFD_EINVAL, "%s: layer %d fans %lld x %lld outside [1, 2^20]", fn, l, (long long)y.fan_in,
+                  (long long)y.fan_out);
+    if (y.fan_in * y.fan_out >= big || d->batch * y.fan_in >= big || d->batch * y.fan_out >= big)
+      return fail(TFD_EINVAL, "%s: layer %d too large", fn, l);
+    if (l > 0 && y.fan_in != d->layer[l - 1].fan_out)
+      return fail(TFD_EINVAL, "%s: layer %d fan_in %lld != fan_out %lld of layer %d", fn, l, (long long)y.fan_in,
+                  (long long)d->layer[l - 1].fan_out, l - 1);
+    if (!y.weights || !y.bias || !y.activations || !y.weight_grad || !y.bias_grad)
+      return fail(TFD_EINVAL, "%s: layer %d: NULL buffer", fn, l);
+    if (y.relu && !y.backprop) return fail(TFD_EINVAL, "%s: layer %d has a Relu but no backprop buffer", fn, l);
+    if (l < L - 1 && !y.relu) return fail(TFD_EUNSUPPORTED, "%s: hidden layer %d without a Relu", fn, l);
+  }
+  if (!d->x || !d->cost_grad || !d->loss) return fail(TFD_EINVAL, "%s: NULL x, cost_grad or loss", fn);
+  if (d->cost == TFD_COST_SOFTMAX_XENT && !d->labels) return fail(TFD_EINVAL, "%s: softmax cost without labels", fn);
+  if (out) {
+    *out = tfd::MlpStep{};
+    out->layers = L;
+    out->cost = d->cost;
+    out->update = d->update != 0;
+    out->batch = d->batch;
+    for (int l = 0; l < L; ++l) {
+      const tfd_mlp_layer& y = d->layer[l];
+      out->fan_in[l] = y.fan_in;
+      out->fan_out[l] = y.fan_out;
+      out->relu[l] = y.relu != 0;
+      out->w[l] = y.weights;
+      out->b[l] = y.bias;
+      out->h[l] = y.activations;
+      out->dy[l] = y.relu ? y.backprop : nullptr;
+      out->dw[l] = y.weight_grad;
+      out->db[l] = y.bias_grad;
+    }
+    out->x = d->x;
+    out->dx0 = d->input_grad;
+    out->g = d->cost_grad;
+    out->target = d->cost == TFD_COST_SQUARED_ERROR ? d->target : nullptr;
+    out->labels = d->cost == TFD_COST_SOFTMAX_XENT ? d->labels : nullptr;
+    out->loss = d->loss;
+    out->lr = d->learning_rate;
+  }
+  return TFD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tfd_mlp_step_workspace_size(const tfd_mlp_step_desc* desc) {
+  if (mlp_check(desc, "tfd_mlp_step_workspace_size", nullptr) != TFD_OK) return 0;
+  return tfd::mlp_step_ws_bytes(desc->batch, desc->layer[desc->layers - 1].fan_out, desc->cost);
+}
+
+tfd_status tfd_mlp_step(const tfd_mlp_step_desc* desc, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err[0] = 0;
+  tfd::MlpStep st;
+  const tfd_status c = mlp_check(desc, "tfd_mlp_step", &st);
+  if (c != TFD_OK) return c;
+  if (st.batch == 0) return TFD_OK;
+  const size_t need = tfd::mlp_step_ws_bytes(st.batch, st.fan_out[st.layers - 1], st.cost);
+  if (!workspace || workspace_bytes < need)
+    return fail(TFD_EINVAL, "tfd_mlp_step: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 7) return fail(TFD_EINVAL, "tfd_mlp_step: workspace not 8-byte aligned");
+  return hip_status(tfd::launch_mlp_step(st, workspace, as_stream(stream)), "tfd_mlp_step launch");
+}
+
+}  // extern "C"

@@ -92,6 +92,31 @@ hipError_t static_scratch(void** out);
 // Engine clock probe: counters[0] = shader clock cycles, counters[1] = 100 MHz
 // real-time ticks over the same run of `iterations` dependent FMAs.
 hipError_t launch_clock_probe(uint64_t* counters, int64_t iterations, hipStream_t s);
+// One training step of a small fp32 MLP in one persistent kernel (the
+// layers' buffers as in tfd_mlp_step_desc; validated by the caller).
+constexpr int kMlpMaxLayers = 4;
+constexpr size_t kMlpCtlBytes = 4096;  // barrier words at the start of the workspace
+struct MlpStep {
+  int layers, cost, update;
+  int64_t batch;
+  int64_t fan_in[kMlpMaxLayers], fan_out[kMlpMaxLayers];
+  int relu[kMlpMaxLayers];
+  float* w[kMlpMaxLayers];
+  float* b[kMlpMaxLayers];
+  float* h[kMlpMaxLayers];
+  float* dy[kMlpMaxLayers];
+  float* dw[kMlpMaxLayers];
+  float* db[kMlpMaxLayers];
+  const float* x;
+  float* dx0;
+  float* g;
+  const float* target;
+  const int32_t* labels;
+  double* loss;
+  float lr;
+};
+size_t mlp_step_ws_bytes(int64_t batch, int64_t classes, int cost);
+hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s);
 // The same with the Relu test read from a bit mask (rows x ldm words).
 hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,
                                                float* db, int64_t rows, int64_t cols, bool bf16, void* ws,

@@ -38,7 +38,26 @@ EXPORTS = (
     "tfd_relu_mask", "tfd_matmul_relu_mask", "tfd_relu_mask_grad_bias_add_grad",
     "tfd_matmul_relu_mask_grad_bias_add_grad", "tfd_matmul_workspace_size", "tfd_matmul_with_workspace",
     "tfd_set_tuning", "tfd_relu_grad_bias_add_grad_noalloc", "tfd_clock_probe",
+    "tfd_mlp_step_workspace_size", "tfd_mlp_step",
 )
+
+MLP_MAX_LAYERS = 4
+COSTS = {"sq_err": 0, "softmax_xent": 1}
+
+
+class MlpLayer(ctypes.Structure):
+    """tfd_mlp_layer (include/tfdense.h)."""
+    _fields_ = [("weights", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("activations", ctypes.c_void_p),
+                ("backprop", ctypes.c_void_p), ("weight_grad", ctypes.c_void_p), ("bias_grad", ctypes.c_void_p),
+                ("fan_in", ctypes.c_int64), ("fan_out", ctypes.c_int64), ("relu", ctypes.c_int32)]
+
+
+class MlpStepDesc(ctypes.Structure):
+    """tfd_mlp_step_desc (include/tfdense.h)."""
+    _fields_ = [("layers", ctypes.c_int32), ("batch", ctypes.c_int64), ("x", ctypes.c_void_p),
+                ("input_grad", ctypes.c_void_p), ("layer", MlpLayer * MLP_MAX_LAYERS), ("cost", ctypes.c_int32),
+                ("target", ctypes.c_void_p), ("labels", ctypes.c_void_p), ("cost_grad", ctypes.c_void_p),
+                ("loss", ctypes.c_void_p), ("learning_rate", ctypes.c_float), ("update", ctypes.c_int32)]
 
 
 class TfdError(RuntimeError):
@@ -101,6 +120,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
         "tfd_set_tuning": ([ctypes.c_char_p, i32], i32),
         "tfd_relu_grad_bias_add_grad_noalloc": ([vp, vp, vp, vp, i64, i64, i32, vp], i32),
         "tfd_clock_probe": ([vp, i64, vp], i32),
+        "tfd_mlp_step_workspace_size": ([ctypes.POINTER(MlpStepDesc)], sz),
+        "tfd_mlp_step": ([ctypes.POINTER(MlpStepDesc), vp, sz, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -515,6 +536,47 @@ def tfd_convert_bf16_to_f32(src, dst, stream=None):
         raise ValueError("src must be bfloat16 and dst contiguous fp32 of the same size")
     _check(load().tfd_convert_bf16_to_f32(_ptr(src), _ptr(dst), n, _stream(stream)))
     return dst
+
+
+def mlp_step_desc(x, layers, cost, cost_grad, loss, target=None, labels=None, input_grad=None,
+                  learning_rate=0.01, update=True):
+    """A tfd_mlp_step_desc over fp32 device tensors. ``layers``: one dict per
+    layer with weights, bias, activations, backprop (or None), weight_grad,
+    bias_grad and relu; ``cost``: "sq_err" or "softmax_xent". The tensors must
+    stay alive while the descriptor is used."""
+    if len(layers) > MLP_MAX_LAYERS:
+        raise ValueError(f"at most {MLP_MAX_LAYERS} layers")
+    d = MlpStepDesc()
+    d.layers = len(layers)
+    d.batch = x.shape[0]
+    d.x = _ptr(x)
+    d.input_grad = _ptr(input_grad) if input_grad is not None else None
+    for i, ly in enumerate(layers):
+        w = ly["weights"]
+        d.layer[i] = MlpLayer(_ptr(w), _ptr(ly["bias"]), _ptr(ly["activations"]),
+                              _ptr(ly["backprop"]) if ly.get("backprop") is not None else None,
+                              _ptr(ly["weight_grad"]), _ptr(ly["bias_grad"]), w.shape[0], w.shape[1],
+                              1 if ly["relu"] else 0)
+    d.cost = COSTS[cost]
+    d.target = _ptr(target) if target is not None else None
+    d.labels = _ptr(labels) if labels is not None else None
+    d.cost_grad = _ptr(cost_grad)
+    d.loss = _ptr(loss)
+    d.learning_rate = float(learning_rate)
+    d.update = 1 if update else 0
+    return d
+
+
+def tfd_mlp_step_workspace_size(desc):
+    return int(load().tfd_mlp_step_workspace_size(ctypes.byref(desc)))
+
+
+def tfd_mlp_step(desc, workspace, stream=None):
+    """One whole training step of a small fp32 MLP in one kernel (see the
+    header); ``workspace``: a uint8 device tensor whose first 256 bytes are
+    zero before its first use."""
+    _check(load().tfd_mlp_step(ctypes.byref(desc), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                               _stream(stream)))
 
 
 def tfd_clock_probe(counters, iterations, stream=None):

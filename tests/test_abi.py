@@ -240,3 +240,61 @@ def test_matmul_with_workspace_validation_and_plan(lib):
     assert mw(1, 1, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE * 4, 4, 0, None, 0, FAKE * 8, 64, None) == 2
     assert mw(0, 0, 4, 4, 4, FAKE, 4, 0, FAKE * 2, 4, 0, FAKE + 16, 4, 0, None, 0, FAKE * 8, 64, None) == 1
     assert mw(0, 0, 0, 4, 4, None, 4, 0, None, 4, 0, None, 4, 0, None, 0, None, 0, None) == 0
+
+
+def _mlp_desc(dims, relus, batch=256, cost=0, fake=FAKE):
+    import ctypes as C
+
+    from paper_1603_04467_amd import tfdense as T
+    d = T.MlpStepDesc()
+    d.layers = len(dims) - 1
+    d.batch = batch
+    d.x = fake
+    d.input_grad = None
+    for i in range(len(dims) - 1):
+        base = fake * (16 + 8 * i)
+        d.layer[i] = T.MlpLayer(base, base + 0x1000, base + 0x2000, base + 0x3000 if relus[i] else None,
+                                base + 0x4000, base + 0x5000, dims[i], dims[i + 1], 1 if relus[i] else 0)
+    d.cost = cost
+    d.target = None
+    d.labels = fake * 3 if cost == 1 else None
+    d.cost_grad = fake * 5
+    d.loss = fake * 6
+    d.learning_rate = C.c_float(0.01)
+    d.update = 1
+    return d
+
+
+def test_fused_step_validation(lib):
+    """tfd_mlp_step: the descriptor is read field by field (the workspace size
+    follows the cost head's item count) and rejected before any launch."""
+    import ctypes as C
+    step = lib.tfd_mlp_step
+    size = lib.tfd_mlp_step_workspace_size
+    d = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0))
+    # 4096 control bytes + one float64 partial per 1024 elements of G (256 x 10)
+    assert size(C.byref(d)) == 4096 + 8 * 3
+    dx = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0), cost=1)
+    assert size(C.byref(dx)) == 4096 + 8 * 64                   # one partial per 4 rows
+    assert step(C.byref(d), FAKE * 9, 4096 + 8 * 3 - 1, None) == 1
+    assert b"workspace" in lib.tfd_last_error()
+    assert step(C.byref(d), FAKE * 9 + 4, 8192, None) == 1      # misaligned
+    bad = _mlp_desc((784, 1024, 1024, 10), (1, 0, 0))           # hidden layer without Relu
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 2
+    bad = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0))
+    bad.layer[1].fan_in = 1000                                  # fans do not chain
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 1 and b"fan_in" in lib.tfd_last_error()
+    bad = _mlp_desc((784, 100), (1,))
+    bad.layer[0].backprop = None                                # Relu layer without dY buffer
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 1
+    bad = _mlp_desc((784, 100), (1,), cost=1)
+    bad.labels = None
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 1
+    bad = _mlp_desc((784, 100), (1,))
+    bad.layers = 5
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 1 and size(C.byref(bad)) == 0
+    bad = _mlp_desc((784, 100), (1,), batch=-1)
+    assert step(C.byref(bad), FAKE * 9, 8192, None) == 1
+    assert step(None, FAKE * 9, 8192, None) == 1
+    empty = _mlp_desc((784, 100), (1,), batch=0)
+    assert step(C.byref(empty), None, 0, None) == 0              # nothing to do
