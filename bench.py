@@ -26,8 +26,8 @@ check. Per workload:
      (sum of 2 m n k) / ms_per_step; roofline.achieved = the dominant
      kernel's FLOPs per launch / its mean launch interval in this pass.
 The MNIST-shaped steps are launch-bound: their value comes from the fastest
-of four unmarked launch modes (one stream, several streams, HIP graph
-replay of either).
+unmarked launch mode (one stream, several streams, HIP graph replay of
+either, the one-kernel step).
 
 The cpu_baseline leg times the oracle (float64 numpy) on bounded row samples
 of every workload on the host cores, and compares the oracle's row-local
@@ -324,11 +324,13 @@ def _gpu_rows(s, rows):
 
 
 def time_modes(s, steps: int, warmup: int, num_streams: int = 3):
-    """Step time under four launch modes, without per-op events: one stream
+    """Step time under the launch modes, without per-op events: one stream
     in program order ("serial"), independent ops on `num_streams` streams
-    ("streams"), and both captured into a HIP graph and replayed ("graph",
-    "graph_streams"). Every step starts from the same Variables (restore
-    outside the timed interval); times are HIP-event means in ms."""
+    ("streams"), both captured into a HIP graph and replayed ("graph",
+    "graph_streams"), and, where the step qualifies, the whole step as one
+    persistent kernel ("fused", tfd_mlp_step). Every step starts from the
+    same Variables (restore outside the timed interval); times are HIP-event
+    means in ms."""
     import torch
 
     stream = torch.cuda.current_stream()
@@ -340,6 +342,8 @@ def time_modes(s, steps: int, warmup: int, num_streams: int = 3):
         "graph": graphs["graph"].replay,
         "graph_streams": graphs["graph_streams"].replay,
     }
+    if s.fusable():
+        modes["fused"] = s.run_fused
     out = {}
     for mode, fn in modes.items():
         for _ in range(warmup):

@@ -298,6 +298,71 @@ class DenseStep:
         from and joined back to the current stream."""
         self.executor(num_streams).enqueue(torch.cuda.current_stream())
 
+    def fusable(self) -> bool:
+        """Whether the whole step can run as one tfd_mlp_step kernel: fp32,
+        at most four layers, a Relu on every hidden layer, a squared-error or
+        softmax cost head, the fused program (dX of a layer above a Relu folded
+        into the ReluGrad below it), no masks."""
+        w = self.w
+        return (w.act == "f32" and w.layers <= T.MLP_MAX_LAYERS and all(w.relus[:-1]) and self.fuse
+                and not self.use_masks and w.cost in ("sq_err", "half_sq", "xent") and self.upstream is None)
+
+    def _fused_desc(self):
+        if "_fdesc" not in self.__dict__:
+            w, L = self.w, self.w.layers
+            layers = [{"weights": self.weights[l], "bias": self.biases[l], "activations": self.h[l + 1],
+                       "backprop": self.dy[l], "weight_grad": self.dw[l], "bias_grad": self.db[l],
+                       "relu": w.relus[l]} for l in range(L)]
+            cost = "softmax_xent" if w.cost == "xent" else "sq_err"
+            self._fdesc = T.mlp_step_desc(self.x, layers, cost, self.g, self.loss, target=self.target,
+                                          labels=self.labels, input_grad=self.dx[0], learning_rate=w.lr,
+                                          update=w.update)
+            # the first 4096 bytes (the kernel's grid barrier) start at zero;
+            # every completed step leaves its counters and error word at zero
+            self._fws = torch.zeros(T.tfd_mlp_step_workspace_size(self._fdesc), dtype=torch.uint8, device=self.device)
+        return self._fdesc
+
+    def run_fused(self, stream=None):
+        """Enqueue the whole step as one persistent kernel (tfd_mlp_step);
+        the same tensors as run() are written."""
+        if not self.fusable():
+            raise ValueError(f"{self.w.name}: the one-kernel step needs fp32, <= {T.MLP_MAX_LAYERS} layers, "
+                             "Relu hidden layers, a squared-error or softmax cost and the fused program")
+        d = self._fused_desc()
+        T.tfd_mlp_step(d, self._fws, stream=stream)
+
+    def fused_barrier_error(self) -> int:
+        """The fused kernel's barrier error word (nonzero: a wait timed out)."""
+        if "_fws" not in self.__dict__:
+            return 0
+        return int(self._fws[0:4].view(torch.int32).item())
+
+    @property
+    def launch_mode(self) -> str:
+        """The default way to run this step, from measurements on MI355X: for
+        steps whose MatMuls are too small to fill the GPU one at a time
+        (every activation under 2^22 elements), the step captured once into a
+        HIP graph and replayed (784x100: 0.040 ms against 0.050 in program
+        order; the 784-1024-1024-10 MLP within 5% of program order, 0.13 ms);
+        else the kernels in program order on one stream. The one-kernel step
+        (run_fused) is correct but slower on both (0.059 and 0.26 ms): its
+        eight grid-wide barriers cost about 8 us each and its latency-bound
+        tiles run longer than the per-op kernels'."""
+        w = self.w
+        return "graph" if w.batch * max(w.dims) <= (1 << 22) else "serial"
+
+    def step(self, stream=None):
+        """One step in this step's default launch mode (launch_mode); the
+        graph is captured on the first call."""
+        if self.launch_mode == "graph":
+            if "_graph" not in self.__dict__:
+                self._graph = self.capture(concurrent=False)
+            st = stream or torch.cuda.current_stream()
+            with torch.cuda.stream(st):
+                self._graph.replay()
+        else:
+            self.run(stream=stream)
+
     def capture(self, concurrent=True, num_streams=3):
         """Record one step into a HIP graph (torch.cuda.CUDAGraph); replaying
         it runs the same kernels on the same buffers. The library's calls

@@ -105,3 +105,30 @@ def test_repeated_concurrent_steps_chain_correctly():
     torch.cuda.synchronize()
     _assert_same(_state(a), _state(b), "three chained steps")
     assert np.isfinite(a.loss.item())
+
+
+@pytest.mark.parametrize("name,batch,dims", CASES)
+@pytest.mark.parametrize("mode", ["streams", "graph", "graph_streams"])
+def test_concurrent_and_graph_outputs_match_the_oracle(name, batch, dims, mode):
+    """The multi-stream step and the graph replays checked against the oracle
+    directly (not only against the serial step): the whole chain from the
+    seeded inputs, and every op teacher-forced on the GPU's own operands."""
+    from tests.teacher import check_step
+    from tests.test_gpu_step import _compare_full
+
+    w = _workload(name, batch, dims)
+    inp = workloads.generate(w, seed=3)
+    s = DenseStep(w, inp)
+    g = None
+    if mode != "streams":
+        g = s.capture(concurrent=mode == "graph_streams", num_streams=3)
+    for rep in range(2):
+        s.restore()
+        if g is None:
+            s.run_concurrent(3)
+        else:
+            g.replay()
+        torch.cuda.synchronize()
+        _compare_full(w, inp, s)
+        check_step(s)
+    del g
