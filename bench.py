@@ -297,6 +297,7 @@ def time_workload(name: str, steps: int, warmup: int, keep_rows: int = 0, clock:
             "src": KERNEL_SOURCES[w.act],
         },
         "loss": float(s.loss.item()),
+        "invariants": invariants(s),
     }
     if keep_rows:
         out["gpu_rows"] = _gpu_rows(s, keep_rows)
@@ -304,6 +305,38 @@ def time_workload(name: str, steps: int, warmup: int, keep_rows: int = 0, clock:
         out["launch_modes"] = time_modes(s, steps, warmup)
     del s
     torch.cuda.empty_cache()
+    return out
+
+
+def invariants(s):
+    """Identities the step's own tensors (from the timed pass) must satisfy,
+    counted on the GPU in full (measurement only): ReLU masks equal the signs
+    of the stored activations; a ReluGrad output is +0 wherever its layer's
+    activation is not > 0; each bias gradient equals the column sums of its dY within the fp32 sum
+    bound 2 N 2^-24 sum|dY| (reported as the largest ratio to that bound)."""
+    import torch
+
+    w, L = s.w, s.w.layers
+    out = {"mask_bit_mismatches": 0, "relugrad_nonzero_where_inactive": 0}
+    for l in range(L):
+        h = s.h[l + 1]
+        if s.masks[l] is not None and h.shape[1] % 32 == 0:
+            bits = (h > 0).view(h.shape[0], -1, 32).to(torch.int64)
+            words = (bits << torch.arange(32, device=h.device)).sum(dim=2)
+            got = s.masks[l][:, :words.shape[1]].to(torch.int64) & 0xFFFFFFFF
+            out["mask_bit_mismatches"] += int((got != words).sum().item())
+        if w.relus[l] and s.dy[l] is not None:
+            dy = s.dy_of(l)
+            bad = (h <= 0) & ((dy != 0) | torch.signbit(dy))
+            out["relugrad_nonzero_where_inactive"] += int(bad.sum().item())
+    worst = 0.0
+    for l in range(L):
+        dy = s.dy_of(l).double()
+        col = dy.sum(dim=0)
+        bound = 2.0 * w.batch * 2.0 ** -24 * dy.abs().sum(dim=0) + 2.0 ** -24 * col.abs()
+        r = ((s.db[l].double() - col).abs() / bound.clamp_min(1e-300)).max().item()
+        worst = max(worst, r)
+    out["db_colsum_ratio_to_bound"] = round(worst, 4)
     return out
 
 
@@ -625,6 +658,9 @@ def _per_op(ops):
             d["tflops"] = round(v["tflops"], 1)
             d["kernel"] = v["kernel"]
             d["algorithmic_bytes"] = v["algorithmic_bytes"]
+            t = lookup_traffic(v["kernel"], v["kernel"].split()[1])
+            if t is not None:
+                d["traffic_bytes"] = round(t["bytes"])
         if "gbs" in v:
             d["gbs"] = round(v["gbs"], 1)
         out[k] = d
@@ -642,6 +678,7 @@ def _entry(name, r):
         "roofline": r["roofline"],
         "per_op": _per_op(r["ops"]),
         "loss": r["loss"],
+        "invariants": r["invariants"],
     }
     if "launch_modes" in r:
         lm = r["launch_modes"]
@@ -712,6 +749,7 @@ def main():
         "per_op": _per_op(r["ops"]),
         "sclk_mhz": r["clock"],
         "loss": r["loss"],
+        "invariants": r["invariants"],
         "revision": revision(),
     }
     if not args.no_secondary and args.workload == PRIMARY:
