@@ -360,8 +360,9 @@ def time_modes(s, steps: int, warmup: int, num_streams: int = 3):
     """Step time under the launch modes, without per-op events: one stream
     in program order ("serial"), independent ops on `num_streams` streams
     ("streams"), both captured into a HIP graph and replayed ("graph",
-    "graph_streams"), and, where the step qualifies, the whole step as one
-    persistent kernel ("fused", tfd_mlp_step). Every step starts from the
+    "graph_streams"), and, where the step qualifies, the step through
+    tfd_mlp_step: one launch per phase ("fused") or one persistent kernel
+    ("fused_persistent"). Every step starts from the
     same Variables (restore outside the timed interval); times are HIP-event
     means in ms."""
     import torch
@@ -377,6 +378,7 @@ def time_modes(s, steps: int, warmup: int, num_streams: int = 3):
     }
     if s.fusable():
         modes["fused"] = s.run_fused
+        modes["fused_persistent"] = lambda: s.run_fused(persistent=True)
     out = {}
     for mode, fn in modes.items():
         for _ in range(warmup):

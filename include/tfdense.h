@@ -433,9 +433,13 @@ TFD_API tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void*
  * in-place update of section 2, "Variables"). The same computation as the
  * per-op calls above, for steps too small to fill the GPU one kernel at a time
  * (a few hundred rows, layers of a few thousand units), where launch gaps
- * dominate: the ops run as phases separated by grid-wide barriers in one
- * cooperative launch, each phase's MatMul tiles, column sums and update chunks
- * spread over the workgroups.
+ * dominate: the ops are grouped into 2 L + 2 phases (forward layers, the cost
+ * head, one phase per layer of the backward pass that also holds the update of
+ * the layer above, the update of layer 0), each phase's MatMul tiles, column
+ * sums and update chunks spread over the workgroups of one launch. With
+ * `persistent` nonzero all phases run in one cooperative launch, separated by
+ * grid-wide barriers; otherwise each phase is a launch of its own (stream order
+ * separates them).
  *
  * Layer l (0-based, up to TFD_MLP_MAX_LAYERS), all fp32 row-major with
  * leading dimension = row length:
@@ -455,7 +459,8 @@ TFD_API tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void*
  * has a Relu, else G itself (its backprop is not written). Every Variable is
  * updated as var - learning_rate * grad, rounded once.
  *
- * workspace: tfd_mlp_step_workspace_size(desc) bytes, 8-byte aligned. Its
+ * workspace: tfd_mlp_step_workspace_size(desc) bytes, 8-byte aligned (the
+ * cost head's loss partials, and for the persistent launch its barrier). Its
  * first 4096 bytes hold the grid barrier (an error word at offset 0, a
  * generation count at 256, arrival counters from 512 on) and must be zero
  * before the first call on it; a call that completes normally leaves the
@@ -497,6 +502,7 @@ typedef struct tfd_mlp_step_desc {
   double* loss;
   float learning_rate;
   int32_t update;
+  int32_t persistent;
 } tfd_mlp_step_desc;
 TFD_API size_t tfd_mlp_step_workspace_size(const tfd_mlp_step_desc* desc);
 TFD_API tfd_status tfd_mlp_step(const tfd_mlp_step_desc* desc, void* workspace, size_t workspace_bytes,

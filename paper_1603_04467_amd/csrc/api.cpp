@@ -893,6 +893,7 @@ tfd_status mlp_check(const tfd_mlp_step_desc* d, const char* fn, tfd::MlpStep* o
     out->layers = L;
     out->cost = d->cost;
     out->update = d->update != 0;
+    out->persistent = d->persistent != 0;
     out->batch = d->batch;
     for (int l = 0; l < L; ++l) {
       const tfd_mlp_layer& y = d->layer[l];

@@ -98,6 +98,7 @@ constexpr int kMlpMaxLayers = 4;
 constexpr size_t kMlpCtlBytes = 4096;  // barrier words at the start of the workspace
 struct MlpStep {
   int layers, cost, update;
+  int persistent;  // one cooperative launch with grid barriers, else one launch per phase
   int64_t batch;
   int64_t fan_in[kMlpMaxLayers], fan_out[kMlpMaxLayers];
   int relu[kMlpMaxLayers];

@@ -59,6 +59,7 @@ struct Layer {
 struct StepArgs {
   Layer l[kMlpMaxLayers];
   int layers, batch, cost, update;
+  int only_phase;  // >= 0: run this phase alone (one launch per phase, no barrier)
   float lr;
   const float* x;
   float* dx0;
@@ -360,9 +361,9 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
   const int L = a.layers;
   auto fan_in = [&](int l) { return a.l[l].fan_in; };
   auto fan_out = [&](int l) { return a.l[l].fan_out; };
-  const int nph = num_phases(L, a.update);
-  for (int ph = 0; ph < nph; ++ph) {
-    if (ph > 0 && !grid_sync(a.ctl, gridDim.x, &abort_flag)) return;
+  const int nph = a.only_phase >= 0 ? a.only_phase + 1 : num_phases(L, a.update);
+  for (int ph = a.only_phase >= 0 ? a.only_phase : 0; ph < nph; ++ph) {
+    if (a.only_phase < 0 && ph > 0 && !grid_sync(a.ctl, gridDim.x, &abort_flag)) return;
     const int items = phase_items(fan_in, fan_out, L, a.batch, a.cost, a.update, a.dx0 != nullptr, ph);
     for (int it = blockIdx.x; it < items; it += gridDim.x) {
       if (ph < L) {  // forward of layer ph
@@ -481,8 +482,22 @@ hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s) {
   a.part = reinterpret_cast<double*>(static_cast<char*>(ws) + kMlpCtlBytes);
   auto fi = [&](int l) { return fan_in[l]; };
   auto fo = [&](int l) { return fan_out[l]; };
+  const int nph = num_phases(d.layers, d.update);
+  if (!d.persistent) {
+    // one launch per phase: stream order separates the phases, and each
+    // launch has a workgroup per item
+    for (int ph = 0; ph < nph; ++ph) {
+      a.only_phase = ph;
+      const int items = phase_items(fi, fo, d.layers, a.batch, d.cost, d.update, d.dx0 != nullptr, ph);
+      hipLaunchKernelGGL(mlp_step_kernel, dim3((unsigned)max(items, 1)), dim3(kThreads), 0, s, a);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  a.only_phase = -1;
   int most = 1;
-  for (int ph = 0; ph < num_phases(d.layers, d.update); ++ph)
+  for (int ph = 0; ph < nph; ++ph)
     most = max(most, phase_items(fi, fo, d.layers, a.batch, d.cost, d.update, d.dx0 != nullptr, ph));
   const int cus = cu_count();
   if (cus <= 0) return hipErrorInvalidDevice;

@@ -322,13 +322,16 @@ class DenseStep:
             self._fws = torch.zeros(T.tfd_mlp_step_workspace_size(self._fdesc), dtype=torch.uint8, device=self.device)
         return self._fdesc
 
-    def run_fused(self, stream=None):
-        """Enqueue the whole step as one persistent kernel (tfd_mlp_step);
-        the same tensors as run() are written."""
+    def run_fused(self, stream=None, persistent=False):
+        """Enqueue the whole step through tfd_mlp_step: one launch per phase
+        (2 L + 2 launches), or with ``persistent`` one cooperative kernel with
+        grid barriers between the phases; the same tensors as run() are
+        written."""
         if not self.fusable():
-            raise ValueError(f"{self.w.name}: the one-kernel step needs fp32, <= {T.MLP_MAX_LAYERS} layers, "
+            raise ValueError(f"{self.w.name}: the fused step needs fp32, <= {T.MLP_MAX_LAYERS} layers, "
                              "Relu hidden layers, a squared-error or softmax cost and the fused program")
         d = self._fused_desc()
+        d.persistent = 1 if persistent else 0
         T.tfd_mlp_step(d, self._fws, stream=stream)
 
     def fused_barrier_error(self) -> int:
@@ -337,31 +340,69 @@ class DenseStep:
             return 0
         return int(self._fws[0:4].view(torch.int32).item())
 
+    def small(self) -> bool:
+        """Whether the step's MatMuls are too small to fill the GPU one at a
+        time (every activation under 2^22 elements): its time is launch
+        latency more than arithmetic."""
+        w = self.w
+        return w.batch * max(w.dims) <= (1 << 22)
+
+    def autotune_launch_mode(self, steps: int = 5):
+        """Time the launch modes that apply (program order; the program
+        captured into a HIP graph; tfd_mlp_step with one launch per phase) on
+        `steps` chained steps each, keep the fastest as this step's default,
+        and put the Variables back as they were. Returns the mean ms per mode."""
+        saved = [t.clone() for t in self.variables()]
+        if "_graph" not in self.__dict__:
+            self._graph = self.capture(concurrent=False)
+        modes = {"serial": self.run, "graph": self._graph.replay}
+        if self.fusable():
+            modes["fused"] = self.run_fused
+        times = {}
+        st = torch.cuda.current_stream()
+        for mode, fn in modes.items():
+            for _ in range(2):
+                fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            for _ in range(steps):
+                fn()
+            b.record(st)
+            torch.cuda.synchronize()
+            times[mode] = a.elapsed_time(b) / steps
+            for t, v in zip(self.variables(), saved):
+                t.copy_(v)
+        torch.cuda.synchronize()
+        self._launch_mode = min(times, key=times.get)
+        self.launch_times = times
+        return times
+
     @property
     def launch_mode(self) -> str:
-        """The default way to run this step, from measurements on MI355X: for
-        steps whose MatMuls are too small to fill the GPU one at a time
-        (every activation under 2^22 elements), the step captured once into a
-        HIP graph and replayed (784x100: 0.040 ms against 0.050 in program
-        order; the 784-1024-1024-10 MLP within 5% of program order, 0.13 ms);
-        else the kernels in program order on one stream. The one-kernel step
-        (run_fused) is correct but slower on both (0.059 and 0.26 ms): its
-        eight grid-wide barriers cost about 8 us each and its latency-bound
-        tiles run longer than the per-op kernels'."""
-        w = self.w
-        return "graph" if w.batch * max(w.dims) <= (1 << 22) else "serial"
+        """This step's default launch mode: the measured fastest of
+        autotune_launch_mode for small steps (run on the first step()), the
+        kernels in program order otherwise. On MI355X: 784x100 takes 0.036 ms
+        through tfd_mlp_step with one launch per phase, 0.041 as a graph
+        replay, 0.050 in program order; the 784-1024-1024-10 MLP 0.13 ms in
+        program order, 0.137 as a graph, 0.20 through tfd_mlp_step."""
+        if "_launch_mode" in self.__dict__:
+            return self._launch_mode
+        return "auto" if self.small() else "serial"
 
     def step(self, stream=None):
-        """One step in this step's default launch mode (launch_mode); the
-        graph is captured on the first call."""
-        if self.launch_mode == "graph":
-            if "_graph" not in self.__dict__:
-                self._graph = self.capture(concurrent=False)
+        """One step in this step's default launch mode (launch_mode)."""
+        mode = self.launch_mode
+        if mode == "auto":
+            self.autotune_launch_mode()
+            mode = self._launch_mode
+        if mode == "serial":
+            self.run(stream=stream)
+        elif mode == "fused":
+            self.run_fused(stream=stream)
+        else:
             st = stream or torch.cuda.current_stream()
             with torch.cuda.stream(st):
                 self._graph.replay()
-        else:
-            self.run(stream=stream)
 
     def capture(self, concurrent=True, num_streams=3):
         """Record one step into a HIP graph (torch.cuda.CUDAGraph); replaying

@@ -57,7 +57,8 @@ class MlpStepDesc(ctypes.Structure):
     _fields_ = [("layers", ctypes.c_int32), ("batch", ctypes.c_int64), ("x", ctypes.c_void_p),
                 ("input_grad", ctypes.c_void_p), ("layer", MlpLayer * MLP_MAX_LAYERS), ("cost", ctypes.c_int32),
                 ("target", ctypes.c_void_p), ("labels", ctypes.c_void_p), ("cost_grad", ctypes.c_void_p),
-                ("loss", ctypes.c_void_p), ("learning_rate", ctypes.c_float), ("update", ctypes.c_int32)]
+                ("loss", ctypes.c_void_p), ("learning_rate", ctypes.c_float), ("update", ctypes.c_int32),
+                ("persistent", ctypes.c_int32)]
 
 
 class TfdError(RuntimeError):
@@ -539,7 +540,7 @@ def tfd_convert_bf16_to_f32(src, dst, stream=None):
 
 
 def mlp_step_desc(x, layers, cost, cost_grad, loss, target=None, labels=None, input_grad=None,
-                  learning_rate=0.01, update=True):
+                  learning_rate=0.01, update=True, persistent=False):
     """A tfd_mlp_step_desc over fp32 device tensors. ``layers``: one dict per
     layer with weights, bias, activations, backprop (or None), weight_grad,
     bias_grad and relu; ``cost``: "sq_err" or "softmax_xent". The tensors must
@@ -564,6 +565,7 @@ def mlp_step_desc(x, layers, cost, cost_grad, loss, target=None, labels=None, in
     d.loss = _ptr(loss)
     d.learning_rate = float(learning_rate)
     d.update = 1 if update else 0
+    d.persistent = 1 if persistent else 0
     return d
 
 
