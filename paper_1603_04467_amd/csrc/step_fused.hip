@@ -14,7 +14,7 @@
 //                   no Relu);
 //   cost            G, the loss partials, and dY of the output layer
 //                   (ReluGrad of G when that layer has a Relu);
-//   B_{L-1} .. B_0  dW_l = H_l^T dY_l, db_l = column sums of dY_l, and
+//   B_{L-1} .. B_0  dW_l = H_l^T dY_l (64 x 64 tiles), db_l = column sums of dY_l, and
 //                   dY_{l-1} = ReluGrad(dY_l W_l^T, H_l) (the input gradient
 //                   dX_0 = dY_0 W_0^T for l = 0, when asked for); the update
 //                   of layer l + 1, whose weights B_{l+1} was the last to read;
@@ -40,11 +40,13 @@ namespace tfd {
 
 namespace {
 
-constexpr int kThreads = 256;  // 4 waves: one 32 x 32 tile, k split 4 ways
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;  // one 32 x 32 tile, k split 4 ways
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kSgdChunk = 4096;   // elements per update item
 constexpr int kCostChunk = 1024;  // elements per squared-error item
-constexpr int kXentRows = 4;      // rows per cross-entropy item (one per wave)
+constexpr int kXentRows = kWaves;  // rows per cross-entropy item (one per wave)
+constexpr int kColsumCols = 32;   // columns per bias-gradient item
 
 struct Layer {
   float* w;
@@ -75,6 +77,7 @@ struct StepArgs {
 // (shared with the host, which sizes the grid and the workspace from them)
 
 __host__ __device__ inline int tiles32(int m, int n) { return ((m + 31) / 32) * ((n + 31) / 32); }
+__host__ __device__ inline int tiles64(int m, int n) { return ((m + 63) / 64) * ((n + 63) / 64); }
 __host__ __device__ inline int chunks(int64_t count, int chunk) { return (int)((count + chunk - 1) / chunk); }
 
 __host__ __device__ inline int cost_items(int batch, int classes, int cost) {
@@ -96,7 +99,7 @@ __host__ __device__ inline int phase_items(FI fan_in, FO fan_out, int layers, in
   if (ph == L) return cost_items(batch, fan_out(L - 1), cost);
   if (ph <= 2 * L) {
     const int l = 2 * L - ph;
-    int n = tiles32(fan_in(l), fan_out(l)) + chunks(fan_out(l), kThreads);
+    int n = tiles64(fan_in(l), fan_out(l)) + chunks(fan_out(l), kColsumCols);
     if (l > 0 || dx0) n += tiles32(batch, fan_in(l));
     if (update && l + 1 < L) n += update_items(fan_in(l + 1), fan_out(l + 1));
     if (l == L - 1) n += 1;
@@ -133,14 +136,15 @@ __device__ __forceinline__ void mm_k(const Mm& j, int row, int col, int kb, int 
     small_tile::tile_k<TA, TB, false>(j.a, j.lda, j.b, j.ldb, row, col, kb, ke, h, acc);
 }
 
-// One 32 x 32 tile `t` of job `j` (row-major tiles), with its epilogue.
+// One 32 x 32 tile `t` of job `j` (row-major tiles), with its epilogue: each
+// wave sums a 1 / kWaves share of k; the partial tiles are added in wave order.
 __device__ void mm_tile(const Mm& j, int t, float* part) {
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, h = lane >> 5;
   const int tn = (j.n + 31) / 32;
   const int m0 = (t / tn) * 32, n0 = (t % tn) * 32;
   const int row = min(m0 + l32, j.m - 1), col = min(n0 + l32, j.n - 1);
-  int kper = (((j.k + 3) / 4 + 7) / 8) * 8;
+  int kper = (((j.k + kWaves - 1) / kWaves + 7) / 8) * 8;
   if (kper == 0) kper = 8;
   const int kb = w * kper, ke = min(j.k, kb + kper);
   f32x16 acc;
@@ -157,9 +161,9 @@ __device__ void mm_tile(const Mm& j, int t, float* part) {
   for (int e = threadIdx.x; e < 1024; e += kThreads) {
     const int gr = m0 + (e >> 5), gc = n0 + (e & 31);
     if (gr < j.m && gc < j.n) {
-      float v = part[e] + part[1024 + e];
-      v += part[2048 + e];
-      v += part[3072 + e];
+      float v = part[e];
+#pragma unroll
+      for (int q = 1; q < kWaves; ++q) v += part[q * 1024 + e];
       if (j.epi == 1) {
         v += j.bias[gc];
         if (j.relu) v = relu_f32(v);
@@ -173,18 +177,74 @@ __device__ void mm_tile(const Mm& j, int t, float* part) {
   __syncthreads();
 }
 
+// One 64 x 64 tile `t` of a plain job (row-major tiles): wave q sums k for the
+// 32 x 32 quadrant q (q / 2, q % 2) (with 8 waves, waves q and q + 4 the two
+// halves of k, the second half's partial added through LDS) and stores
+// straight from its accumulators (each register is one row's 32
+// consecutive columns across a half-wave). For the weight gradients (k =
+// batch, both operands m/n-contiguous): a quarter as many tiles as 32 x 32
+// ones, each wave with a longer loop over which its loads overlap.
+__device__ void mm_tile64(const Mm& j, int t, float* part) {
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l32 = lane & 31, h = lane >> 5;
+  const int q = w & 3, kh = w >> 2;
+  const int tn = (j.n + 63) / 64;
+  const int m0 = (t / tn) * 64 + (q >> 1) * 32, n0 = (t % tn) * 64 + (q & 1) * 32;
+  const bool live = m0 < j.m && n0 < j.n;
+  const int row = min(m0 + l32, j.m - 1), col = min(n0 + l32, j.n - 1);
+  // with 8 waves the two halves of k go to waves q and q + 4; with 4, one wave
+  // per quadrant takes all of k
+  const int kmid = kWaves == 8 ? min(j.k, ((j.k / 2 + 7) / 8) * 8) : j.k;
+  const int kb = kh ? kmid : 0, ke = kh ? j.k : kmid;
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  if (live) {
+    if (j.ta)
+      mm_k<true, false>(j, row, col, kb, ke, h, acc);
+    else if (j.tb)
+      mm_k<false, true>(j, row, col, kb, ke, h, acc);
+    else
+      mm_k<false, false>(j, row, col, kb, ke, h, acc);
+  }
+  if (kWaves == 8 && kh) small_tile::store_part(part + q * 1024, acc, h, l32);
+  __syncthreads();
+  if (!kh && live) {
+    const int gc = n0 + l32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int er = 8 * (r >> 2) + 4 * h + (r & 3);
+      const int gr = m0 + er;
+      if (gr < j.m && gc < j.n) j.c[(int64_t)gr * j.ldc + gc] = kWaves == 8 ? acc[r] + part[q * 1024 + er * 32 + l32] : acc[r];
+    }
+  }
+  __syncthreads();
+}
+
 __device__ __forceinline__ float relu_grad(float g, float f) {
   return __builtin_bit_cast(float, f > 0.0f ? __builtin_bit_cast(uint32_t, g) : 0u);
 }
 
-// Column sums of x [rows, cols] for columns item * 256 + thread, rows in order.
-__device__ void colsum_item(const float* x, float* out, int rows, int cols, int item) {
-  const int c = item * kThreads + threadIdx.x;
-  if (c < cols) {
-    float s = 0.0f;
-    for (int r = 0; r < rows; ++r) s += x[(int64_t)r * cols + c];
-    out[c] = s;
+// Column sums of x [rows, cols] for the kColsumCols columns of `item`: thread
+// (c, g) sums rows g * span .. of column c (span = ceil(rows / groups)), in
+// order; the partials of a column are then added in g order.
+__device__ void colsum_item(const float* x, float* out, int rows, int cols, int item, float* part) {
+  constexpr int kGroupsR = kThreads / kColsumCols;
+  const int c = item * kColsumCols + (threadIdx.x % kColsumCols), g = threadIdx.x / kColsumCols;
+  const int span = (rows + kGroupsR - 1) / kGroupsR;
+  const int r0 = g * span, r1 = min(rows, r0 + span);
+  float s = 0.0f;
+  if (c < cols)
+    for (int r = r0; r < r1; ++r) s += x[(int64_t)r * cols + c];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x < kColsumCols && c < cols) {
+    float t = part[threadIdx.x];
+#pragma unroll
+    for (int q = 1; q < kGroupsR; ++q) t += part[q * kColsumCols + threadIdx.x];
+    out[c] = t;
   }
+  __syncthreads();
 }
 
 // var[i] <- fma(-lr, delta[i], var[i]) for i in chunk `item` of kSgdChunk:
@@ -355,7 +415,7 @@ __device__ __forceinline__ const float* dy_of(const StepArgs& a, int l) {
 }
 
 __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
-  __shared__ float part[4 * 1024];
+  __shared__ float part[kWaves * 1024];
   __shared__ double red[kThreads];
   __shared__ int abort_flag;
   const int L = a.layers;
@@ -393,17 +453,17 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
           continue;
         }
         r -= n_dx;
-        const int n_dw = tiles32(ly.fan_in, ly.fan_out);
+        const int n_dw = tiles64(ly.fan_in, ly.fan_out);
         if (r < n_dw) {  // dW_l = H_l^T dY_l
           Mm j{act_in(a, l), dy, ly.dw, ly.fan_in, ly.fan_out, ly.fan_out, ly.fan_in, ly.fan_out, a.batch, 1, 0, 0,
                0, nullptr, nullptr};
-          mm_tile(j, r, part);
+          mm_tile64(j, r, part);
           continue;
         }
         r -= n_dw;
-        const int n_db = chunks(ly.fan_out, kThreads);
+        const int n_db = chunks(ly.fan_out, kColsumCols);
         if (r < n_db) {
-          colsum_item(dy, ly.db, a.batch, ly.fan_out, r);
+          colsum_item(dy, ly.db, a.batch, ly.fan_out, r, part);
           continue;
         }
         r -= n_db;
@@ -501,9 +561,13 @@ hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s) {
     most = max(most, phase_items(fi, fo, d.layers, a.batch, d.cost, d.update, d.dx0 != nullptr, ph));
   const int cus = cu_count();
   if (cus <= 0) return hipErrorInvalidDevice;
-  // two workgroups per compute unit: a workgroup's tiles are latency-bound
-  // chains of loads, which the other workgroup's overlap
-  const unsigned grid = (unsigned)min(most, 2 * cus);
+  // up to two workgroups per compute unit (a workgroup's tiles are
+  // latency-bound chains of loads, which the other's overlap), as many as fit
+  int per_cu = 0;
+  const hipError_t oe = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, mlp_step_kernel, kThreads, 0);
+  if (oe != hipSuccess) return oe;
+  if (per_cu < 1) return hipErrorLaunchOutOfResources;
+  const unsigned grid = (unsigned)min(most, min(per_cu, 2) * cus);
   void* args[] = {&a};
   return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(mlp_step_kernel), dim3(grid), dim3(kThreads), args,
                                     0, s);
