@@ -924,7 +924,8 @@ extern "C" {
 
 size_t tfd_mlp_step_workspace_size(const tfd_mlp_step_desc* desc) {
   if (mlp_check(desc, "tfd_mlp_step_workspace_size", nullptr) != TFD_OK) return 0;
-  return tfd::mlp_step_ws_bytes(desc->batch, desc->layer[desc->layers - 1].fan_out, desc->cost);
+  const tfd_mlp_layer& top = desc->layer[desc->layers - 1];
+  return tfd::mlp_step_ws_bytes(desc->batch, top.fan_in, top.fan_out, desc->cost);
 }
 
 tfd_status tfd_mlp_step(const tfd_mlp_step_desc* desc, void* workspace, size_t workspace_bytes, void* stream) {
@@ -933,7 +934,7 @@ tfd_status tfd_mlp_step(const tfd_mlp_step_desc* desc, void* workspace, size_t w
   const tfd_status c = mlp_check(desc, "tfd_mlp_step", &st);
   if (c != TFD_OK) return c;
   if (st.batch == 0) return TFD_OK;
-  const size_t need = tfd::mlp_step_ws_bytes(st.batch, st.fan_out[st.layers - 1], st.cost);
+  const size_t need = tfd::mlp_step_ws_bytes(st.batch, st.fan_in[st.layers - 1], st.fan_out[st.layers - 1], st.cost);
   if (!workspace || workspace_bytes < need)
     return fail(TFD_EINVAL, "tfd_mlp_step: workspace of %zu bytes, %zu needed", workspace_bytes, need);
   if (reinterpret_cast<uintptr_t>(workspace) & 7) return fail(TFD_EINVAL, "tfd_mlp_step: workspace not 8-byte aligned");

@@ -116,7 +116,7 @@ struct MlpStep {
   double* loss;
   float lr;
 };
-size_t mlp_step_ws_bytes(int64_t batch, int64_t classes, int cost);
+size_t mlp_step_ws_bytes(int64_t batch, int64_t top_fan_in, int64_t classes, int cost);
 hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s);
 // The same with the Relu test read from a bit mask (rows x ldm words).
 hipError_t launch_relu_mask_grad_bias_add_grad(const void* g, const uint32_t* mask, int64_t ldm, void* out,

@@ -11,7 +11,9 @@
 // MatMul, column chunks of a BiasAddGrad, chunks of the cost head or of an
 // update) round-robin. Phases, for L layers:
 //   F_0 .. F_{L-1}  H_{l+1} = Relu(H_l W_l + b_l) (identity where the layer has
-//                   no Relu);
+//                   no Relu); an output layer with few tiles over a long k is
+//                   split into k chunks whose partial products the cost phase
+//                   adds (with the bias and the Relu);
 //   cost            G, the loss partials, and dY of the output layer
 //                   (ReluGrad of G when that layer has a Relu);
 //   B_{L-1} .. B_0  dW_l = H_l^T dY_l (64 x 64 tiles), db_l = column sums of dY_l, and
@@ -44,7 +46,7 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;  // one 32 x 32 tile, k split 4 ways
 constexpr uint32_t kSpinLimit = 1u << 22;
 constexpr int kSgdChunk = 4096;   // elements per update item
-constexpr int kCostChunk = 1024;  // elements per squared-error item
+constexpr int kCostChunk = 256;   // elements per squared-error item (one per thread)
 constexpr int kXentRows = kWaves;  // rows per cross-entropy item (one per wave)
 constexpr int kColsumCols = 32;   // columns per bias-gradient item
 
@@ -69,8 +71,10 @@ struct StepArgs {
   const float* target;
   const int32_t* labels;
   double* loss;
-  uint32_t* ctl;  // [0] arrivals, [1] generation, [2] error
+  uint32_t* ctl;  // barrier words (the persistent launch)
   double* part;   // cost phase's loss partials
+  float* split_part;  // output layer's partial products [split][batch][classes]
+  int split;
 };
 
 // ---------------------------------------------------------------- work counts
@@ -78,6 +82,19 @@ struct StepArgs {
 
 __host__ __device__ inline int tiles32(int m, int n) { return ((m + 31) / 32) * ((n + 31) / 32); }
 __host__ __device__ inline int tiles64(int m, int n) { return ((m + 63) / 64) * ((n + 63) / 64); }
+
+// The output layer's forward MatMul over k chunks when its output has few
+// tiles (a narrow classifier layer over a long k): the chunks' partial
+// products go to the workspace and the cost phase adds them, the bias and the
+// Relu before the cost head. Returns the number of chunks (1: no split).
+__host__ __device__ inline int top_split(int batch, int fan_in, int fan_out) {
+  if (tiles32(batch, fan_out) >= 64) return 1;
+  const int s = fan_in / 128;
+  return s < 1 ? 1 : (s > 8 ? 8 : s);
+}
+// k values per chunk: a multiple of 8, so that every chunk starts on a
+// 16-byte boundary of a k-contiguous row
+__host__ __device__ inline int split_chunk(int fan_in, int split) { return (((fan_in + split - 1) / split + 7) / 8) * 8; }
 __host__ __device__ inline int chunks(int64_t count, int chunk) { return (int)((count + chunk - 1) / chunk); }
 
 __host__ __device__ inline int cost_items(int batch, int classes, int cost) {
@@ -95,7 +112,8 @@ template <typename FI, typename FO>
 __host__ __device__ inline int phase_items(FI fan_in, FO fan_out, int layers, int batch, int cost, int update,
                                            bool dx0, int ph) {
   const int L = layers;
-  if (ph < L) return tiles32(batch, fan_out(ph));
+  if (ph < L - 1) return tiles32(batch, fan_out(ph));
+  if (ph == L - 1) return tiles32(batch, fan_out(ph)) * top_split(batch, fan_in(ph), fan_out(ph));
   if (ph == L) return cost_items(batch, fan_out(L - 1), cost);
   if (ph <= 2 * L) {
     const int l = 2 * L - ph;
@@ -115,12 +133,13 @@ struct Mm {
   const float* b;
   float* c;
   int64_t lda, ldb, ldc;
-  int m, n, k;
+  int m, n, k;    // the k range is [kbeg, k)
   int ta, tb;
   int epi;  // 0 plain, 1 bias (+ Relu when relu), 2 ReluGrad against feat
   int relu;
   const float* bias;
   const float* feat;
+  int kbeg;
 };
 
 __device__ __forceinline__ bool aligned16(const void* p, int64_t ld) {
@@ -144,9 +163,9 @@ __device__ void mm_tile(const Mm& j, int t, float* part) {
   const int tn = (j.n + 31) / 32;
   const int m0 = (t / tn) * 32, n0 = (t % tn) * 32;
   const int row = min(m0 + l32, j.m - 1), col = min(n0 + l32, j.n - 1);
-  int kper = (((j.k + kWaves - 1) / kWaves + 7) / 8) * 8;
+  int kper = (((j.k - j.kbeg + kWaves - 1) / kWaves + 7) / 8) * 8;
   if (kper == 0) kper = 8;
-  const int kb = w * kper, ke = min(j.k, kb + kper);
+  const int kb = j.kbeg + w * kper, ke = min(j.k, kb + kper);
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
@@ -279,6 +298,21 @@ __device__ double block_sum_ordered(double v, double* red) {
   return acc;
 }
 
+// Element i of the output layer's activations: with a split forward MatMul,
+// the chunks' partial products added in chunk order, then the bias and the
+// Relu, stored; otherwise as the forward phase stored it.
+__device__ __forceinline__ float top_value(const StepArgs& a, int64_t i) {
+  const Layer& top = a.l[a.layers - 1];
+  if (a.split <= 1) return top.h[i];
+  const int64_t count = (int64_t)a.batch * top.fan_out;
+  float v = a.split_part[i];
+  for (int c = 1; c < a.split; ++c) v += a.split_part[c * count + i];
+  v += top.b[i % top.fan_out];
+  if (top.relu) v = relu_f32(v);
+  top.h[i] = v;
+  return v;
+}
+
 // Squared error over elements [item * kCostChunk, +kCostChunk) of the output:
 // G = out - target (or out), dY = ReluGrad(G, out) for a Relu output layer,
 // and the item's float64 sum of the exact squared differences.
@@ -288,7 +322,7 @@ __device__ void sq_item(const StepArgs& a, int item, double* red) {
   const int64_t i0 = (int64_t)item * kCostChunk;
   double s = 0.0;
   for (int64_t i = i0 + threadIdx.x; i < min(count, i0 + kCostChunk); i += kThreads) {
-    const float o = top.h[i];
+    const float o = top_value(a, i);
     const float t = a.target ? a.target[i] : 0.0f;
     const float d = o - t;
     a.g[i] = d;
@@ -324,7 +358,7 @@ __device__ void xent_item(const StepArgs& a, int item, double* red) {
     const float* zr = top.h + row * cols;
     float* gr = a.g + row * cols;
     float m = -INFINITY;
-    for (int c = lane; c < cols; c += kWave) m = fmaxf(m, zr[c]);
+    for (int c = lane; c < cols; c += kWave) m = fmaxf(m, top_value(a, row * cols + c));
     m = wave_max(m);
     float s = 0.0f;
     for (int c = lane; c < cols; c += kWave) s += expf(zr[c] - m);
@@ -428,8 +462,16 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
     for (int it = blockIdx.x; it < items; it += gridDim.x) {
       if (ph < L) {  // forward of layer ph
         const Layer& ly = a.l[ph];
+        if (ph == L - 1 && a.split > 1) {  // k chunk it / tiles of the output layer: partial product
+          const int tiles = tiles32(a.batch, ly.fan_out), c = it / tiles;
+          const int kc = split_chunk(ly.fan_in, a.split);
+          Mm j{act_in(a, ph), ly.w, a.split_part + (int64_t)c * a.batch * ly.fan_out, ly.fan_in, ly.fan_out,
+               ly.fan_out, a.batch, ly.fan_out, min(ly.fan_in, (c + 1) * kc), 0, 0, 0, 0, nullptr, nullptr, c * kc};
+          mm_tile(j, it - c * tiles, part);
+          continue;
+        }
         Mm j{act_in(a, ph), ly.w, ly.h, ly.fan_in, ly.fan_out, ly.fan_out, a.batch, ly.fan_out, ly.fan_in, 0, 0, 1,
-             ly.relu, ly.b, nullptr};
+             ly.relu, ly.b, nullptr, 0};
         mm_tile(j, it, part);
       } else if (ph == L) {
         if (a.cost == 0)
@@ -448,7 +490,7 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
         if (r < n_dx) {  // dY_{l-1} = ReluGrad(dY_l W_l^T, H_l), or dX_0
           float* out = l > 0 ? a.l[l - 1].dy : a.dx0;
           Mm j{dy, ly.w, out, ly.fan_out, ly.fan_out, ly.fan_in, a.batch, ly.fan_in, ly.fan_out, 0, 1,
-               l > 0 ? 2 : 0, 0, nullptr, l > 0 ? a.l[l - 1].h : nullptr};
+               l > 0 ? 2 : 0, 0, nullptr, l > 0 ? a.l[l - 1].h : nullptr, 0};
           mm_tile(j, r, part);
           continue;
         }
@@ -456,7 +498,7 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
         const int n_dw = tiles64(ly.fan_in, ly.fan_out);
         if (r < n_dw) {  // dW_l = H_l^T dY_l
           Mm j{act_in(a, l), dy, ly.dw, ly.fan_in, ly.fan_out, ly.fan_out, ly.fan_in, ly.fan_out, a.batch, 1, 0, 0,
-               0, nullptr, nullptr};
+               0, nullptr, nullptr, 0};
           mm_tile64(j, r, part);
           continue;
         }
@@ -515,8 +557,15 @@ int cu_count() {
 
 }  // namespace
 
-size_t mlp_step_ws_bytes(int64_t batch, int64_t classes, int cost) {
-  return kMlpCtlBytes + sizeof(double) * (size_t)cost_items((int)batch, (int)classes, cost);
+// [barrier words][loss partials][output layer's split partial products]
+static size_t split_offset(int64_t batch, int64_t classes, int cost) {
+  const size_t b = kMlpCtlBytes + sizeof(double) * (size_t)cost_items((int)batch, (int)classes, cost);
+  return (b + 255) & ~size_t(255);
+}
+
+size_t mlp_step_ws_bytes(int64_t batch, int64_t top_fan_in, int64_t classes, int cost) {
+  const int split = top_split((int)batch, (int)top_fan_in, (int)classes);
+  return split_offset(batch, classes, cost) + (split > 1 ? sizeof(float) * (size_t)split * batch * classes : 0);
 }
 
 hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s) {
@@ -540,6 +589,9 @@ hipError_t launch_mlp_step(const MlpStep& d, void* ws, hipStream_t s) {
   a.loss = d.loss;
   a.ctl = static_cast<uint32_t*>(ws);
   a.part = reinterpret_cast<double*>(static_cast<char*>(ws) + kMlpCtlBytes);
+  const int top = d.layers - 1;
+  a.split = top_split(a.batch, fan_in[top], fan_out[top]);
+  a.split_part = reinterpret_cast<float*>(static_cast<char*>(ws) + split_offset(d.batch, d.fan_out[top], d.cost));
   auto fi = [&](int l) { return fan_in[l]; };
   auto fo = [&](int l) { return fan_out[l]; };
   const int nph = num_phases(d.layers, d.update);

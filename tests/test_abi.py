@@ -272,13 +272,19 @@ def test_fused_step_validation(lib):
     step = lib.tfd_mlp_step
     size = lib.tfd_mlp_step_workspace_size
     d = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0))
-    # 4096 control bytes + one float64 partial per 1024 elements of G (256 x 10)
-    assert size(C.byref(d)) == 4096 + 8 * 3
+    # 4096 control bytes, one float64 loss partial per 256 elements of G
+    # (256 x 10), padded to 256 bytes, then the output layer's forward split
+    # into 8 k chunks of fp32 partial products (8 tiles of 32 x 32 < 64)
+    split = 4 * 8 * 256 * 10
+    assert size(C.byref(d)) == 4352 + split
     dx = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0), cost=1)
-    assert size(C.byref(dx)) == 4096 + 8 * 64                   # one partial per 4 rows
-    assert step(C.byref(d), FAKE * 9, 4096 + 8 * 3 - 1, None) == 1
+    assert size(C.byref(dx)) == 4096 + 8 * 64 + split           # one loss partial per 4 rows
+    wide = _mlp_desc((784, 4096, 4096), (1, 1), batch=512)    # 256 output tiles: no split
+    assert size(C.byref(wide)) == 4096 + 8 * 8192              # 512 x 4096 / 256 loss partials
+    assert step(C.byref(d), FAKE * 9, 4352 + split - 1, None) == 1
     assert b"workspace" in lib.tfd_last_error()
-    assert step(C.byref(d), FAKE * 9 + 4, 8192, None) == 1      # misaligned
+    assert step(C.byref(d), FAKE * 9 + 4, 1 << 20, None) == 1   # misaligned
+    assert b"aligned" in lib.tfd_last_error()
     bad = _mlp_desc((784, 1024, 1024, 10), (1, 0, 0))           # hidden layer without Relu
     assert step(C.byref(bad), FAKE * 9, 8192, None) == 2
     bad = _mlp_desc((784, 1024, 1024, 10), (1, 1, 0))
