@@ -143,7 +143,10 @@ def _clock_probe_mhz(counters):
     return [100.0 * float(r[0]) / float(r[1]) for r in c if r[1] > 0]
 
 
-def sample_clock(s, probes: int = 8, iterations: int = 50_000):
+CLOCK_PROBES = 8
+
+
+def sample_clock(s, probes: int = CLOCK_PROBES, iterations: int = 50_000):
     """Engine clock in MHz, from tfd_clock_probe (shader clock cycles over
     100 MHz real-time ticks in one wave, about 1 ms): `probes` probes each
     enqueued right behind a step (restored Variables, as in the timed pass),
@@ -285,6 +288,10 @@ def time_workload(name: str, steps: int, warmup: int, keep_rows: int = 0, clock:
             "bound": "mfma",
             "kernel": dom_kernel,
             "launches_per_step": len(dom_tags),
+            # the dominant kernel's launches in this workload's leg, in order:
+            # warm-up, per-op pass, timed pass, clock-probe pass
+            "launches_in_leg": len(dom_tags) * (warmup + 2 * steps + (CLOCK_PROBES if clock else 0)),
+            "timed_launches": [len(dom_tags) * (warmup + steps), len(dom_tags) * (warmup + 2 * steps)],
             "ms_per_launch": round(dom_mean, 5),
             "achieved": round(achieved, 2),
             "peak": peak,

@@ -65,8 +65,29 @@ def test_trace_reproduces_the_fraction(tmp_path):
         {"Name": TN, "Calls": 8, "TotalDurationNs": 8 * ns, "AverageNs": ns, "Percentage": 99.0, "MinNs": ns,
          "MaxNs": ns}])
     text = P.trace(str(tmp_path), str(tmp_path / "b.json"))
-    assert "| rocprofv3 kernel trace (every launch in the run) | 8 |" in text
-    assert "0.5000 |" in text and re.search(r"difference of the fractions: [+-]0\.00%", text)
+    assert "| rocprofv3 kernel trace, every launch of the leg | 8 |" in text
+    assert "0.5000 |" in text and re.search(r"difference of the fractions \(bench line vs trace\): [+-]0\.00%", text)
+
+
+def test_trace_selects_the_leg_and_its_timed_pass(tmp_path):
+    """Launches after the bench line's own leg (later workloads reusing the
+    kernel at another k) and outside its timed pass are left out."""
+    ms = _bench(tmp_path / "b.json", frac=0.5)
+    b = json.loads(open(tmp_path / "b.json").read().splitlines()[-1])
+    b["roofline"].update(launches_in_leg=12, timed_launches=[4, 8])
+    open(tmp_path / "b.json", "w").write(json.dumps(b) + "\n")
+    ns = int(ms * 1e6)
+    durs = [3 * ns] * 4 + [ns] * 4 + [2 * ns] * 4 + [ns // 8] * 10    # warm-up, timed, clock pass, another leg
+    trace = [{"Kernel_Name": TN, "Grid_Size_X": 256 * 1024, "Start_Timestamp": 10 ** 7 * i,
+              "End_Timestamp": 10 ** 7 * i + d} for i, d in enumerate(durs)]
+    _write(tmp_path / "run_kernel_trace.csv", trace)
+    _write(tmp_path / "run_kernel_stats.csv", [
+        {"Name": TN, "Calls": len(durs), "TotalDurationNs": sum(durs), "AverageNs": sum(durs) / len(durs),
+         "Percentage": 99.0, "MinNs": min(durs), "MaxNs": max(durs)}])
+    text = P.trace(str(tmp_path), str(tmp_path / "b.json"))
+    assert "| rocprofv3 kernel trace, every launch of the leg | 12 |" in text
+    assert "| rocprofv3 kernel trace, the timed pass | 4 |" in text
+    assert re.search(r"\(bench line vs trace, timed pass\): [+-]0\.00%", text)
 
 
 def test_traffic_records_round_trip(tmp_path, monkeypatch):
