@@ -39,8 +39,6 @@ COPY_BYTES = 64 << 20   # one restore of a 4096 x 4096 fp32 Variable
 _EP_OF = {"none": 0, "bias": 0, "bias_relu": 0, "splitk": 0, "relugrad+colsum": 1, "bias+sq_err+colsum": 2,
           "relugrad_mask+colsum": 3, "bias_relu+mask": 4}
 _EP_NAME = {0: "plain", 1: "ReluGrad(features)", 2: "squared error", 3: "ReluGrad(mask)", 4: "ReLU mask out"}
-# default waves per workgroup of the 16-bit whole-tile kernel by layout
-_WAVES = {"NN": (2, 4), "NT": (2, 4), "TN": (4, 4)}
 
 
 def parse_kernel_id(kid: str) -> dict:
@@ -74,12 +72,17 @@ def _layout(f):
 
 def matches(kid: dict, name: str, grid_threads=None, waves=None) -> bool:
     """Whether kernel symbol `name` (launched with `grid_threads` work-items)
-    is the 16-bit whole-tile kernel of bench kernel id `kid`."""
+    is the 16-bit whole-tile kernel of bench kernel id `kid`. The library picks
+    the waves per workgroup by layout, epilogue and k range; the grid (one
+    workgroup of 64 x waves work-items per 256 x 256 tile) must agree with the
+    symbol's, and with `waves` when given."""
     f = symbol_fields(name)
     if f is None or kid["act"] != "bf16" or kid["epi"] == "splitk":
         return False
-    wm, wn = waves or _WAVES[kid["layout"]]
-    if _layout(f) != kid["layout"] or f["out"] != kid["out"] or f["ep"] != _EP_OF[kid["epi"]] or f["waves"] != (wm, wn):
+    wm, wn = f["waves"]
+    if waves is not None and tuple(waves) != (wm, wn):
+        return False
+    if _layout(f) != kid["layout"] or f["out"] != kid["out"] or f["ep"] != _EP_OF[kid["epi"]]:
         return False
     if grid_threads is not None:
         tiles = (kid["m"] // 256) * (kid["n"] // 256)
@@ -118,8 +121,10 @@ def trace(outdir: str, bench_json: str) -> str:
     b = _bench(bench_json)
     rl = b["roofline"]
     kid = parse_kernel_id(rl["kernel"])
+    hits = [r for r in tr if matches(kid, r["Kernel_Name"], _grid(r))]
     launches = sorted((int(r["Start_Timestamp"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6)
-                      for r in tr if matches(kid, r["Kernel_Name"], _grid(r)))
+                      for r in hits)
+    symbols = sorted({readable(r["Kernel_Name"]) for r in hits})
     # the bench line's own leg comes first in the run (the headline workload
     # is timed before any other): its launches are the first launches_in_leg,
     # and the timed pass is the slice timed_launches of them
@@ -142,7 +147,8 @@ def trace(outdir: str, bench_json: str) -> str:
         ach = rl["flops_per_launch"] / (mean * 1e-3) / 1e12
         return f"| {label} | {len(d)} | {mean:.5f} | {ach:.1f} | {ach / rl['peak']:.4f} |", ach / rl["peak"]
 
-    out += ["", f"Dominant kernel of the bench line: `{rl['kernel']}` ({readable_id(kid)})", "",
+    out += ["", f"Dominant kernel of the bench line: `{rl['kernel']}` ({'; '.join(symbols)}, "
+            f"grid {(kid['m'] // 256) * (kid['n'] // 256)} workgroups)", "",
             "| source | launches | mean ms per launch | achieved TFLOP/s | frac of peak |", "|---|---|---|---|---|"]
     line, frac = row("rocprofv3 kernel trace, every launch of the leg", durs)
     out.append(line)
@@ -154,12 +160,6 @@ def trace(outdir: str, bench_json: str) -> str:
             "", f"difference of the fractions (bench line vs trace{', timed pass' if timed else ''}): "
             f"{100 * (rl['frac'] - frac) / frac:+.2f}%"]
     return "\n".join(out)
-
-
-def readable_id(kid):
-    wm, wn = _WAVES[kid["layout"]]
-    return (f"gemm_bf16_256 {kid['layout']} -> {kid['out']}, {wm * wn} waves, epilogue {_EP_NAME[_EP_OF[kid['epi']]]}, "
-            f"grid {(kid['m'] // 256) * (kid['n'] // 256)} workgroups")
 
 
 def _counter(outdir, counter):
