@@ -16,7 +16,9 @@
 //                   adds (with the bias and the Relu);
 //   cost            G, the loss partials, and dY of the output layer
 //                   (ReluGrad of G when that layer has a Relu);
-//   B_{L-1} .. B_0  dW_l = H_l^T dY_l (64 x 64 tiles), db_l = column sums of dY_l, and
+//   B_{L-1} .. B_0  dW_l = H_l^T dY_l (64 x 64 tiles; 32 x 32 ones with the
+//                   batch split over the waves for a narrow layer), db_l =
+//                   column sums of dY_l, and
 //                   dY_{l-1} = ReluGrad(dY_l W_l^T, H_l) (the input gradient
 //                   dX_0 = dY_0 W_0^T for l = 0, when asked for); the update
 //                   of layer l + 1, whose weights B_{l+1} was the last to read;
@@ -92,6 +94,15 @@ __host__ __device__ inline int top_split(int batch, int fan_in, int fan_out) {
   const int s = fan_in / 128;
   return s < 1 ? 1 : (s > 8 ? 8 : s);
 }
+// The weight gradient's tiles: 64 x 64 (one wave per 32 x 32 quadrant, each
+// over the whole batch) when there are enough of them to fill the chip,
+// else 32 x 32 with the batch split over the waves, so that a narrow layer's
+// few tiles do not each run one long chain of loads (the 1024 x 10 gradient
+// of a 10-class output layer: 16 tiles of 64 x 64, 32 of 32 x 32).
+__host__ __device__ inline bool dw_small_tiles(int fan_in, int fan_out) { return tiles64(fan_in, fan_out) < 64; }
+__host__ __device__ inline int dw_tiles(int fan_in, int fan_out) {
+  return dw_small_tiles(fan_in, fan_out) ? tiles32(fan_in, fan_out) : tiles64(fan_in, fan_out);
+}
 // k values per chunk: a multiple of 8, so that every chunk starts on a
 // 16-byte boundary of a k-contiguous row
 __host__ __device__ inline int split_chunk(int fan_in, int split) { return (((fan_in + split - 1) / split + 7) / 8) * 8; }
@@ -117,7 +128,7 @@ __host__ __device__ inline int phase_items(FI fan_in, FO fan_out, int layers, in
   if (ph == L) return cost_items(batch, fan_out(L - 1), cost);
   if (ph <= 2 * L) {
     const int l = 2 * L - ph;
-    int n = tiles64(fan_in(l), fan_out(l)) + chunks(fan_out(l), kColsumCols);
+    int n = dw_tiles(fan_in(l), fan_out(l)) + chunks(fan_out(l), kColsumCols);
     if (l > 0 || dx0) n += tiles32(batch, fan_in(l));
     if (update && l + 1 < L) n += update_items(fan_in(l + 1), fan_out(l + 1));
     if (l == L - 1) n += 1;
@@ -287,13 +298,25 @@ __device__ void sgd_item(float* var, const float* delta, int64_t count, float lr
   for (int64_t k = i + threadIdx.x; k < i1; k += kThreads) var[k] = __builtin_fmaf(na, delta[k], var[k]);
 }
 
-// Sum of one double per thread, in thread order (thread 0 gets the result).
+// Sum of one double per thread in a fixed order (thread 0 gets the result):
+// kSumRuns runs of consecutive threads, each summed in thread order, then the
+// run sums in order. red holds kThreads + kSumRuns doubles.
+constexpr int kSumRuns = 16;
 __device__ double block_sum_ordered(double v, double* red) {
+  constexpr int kRun = kThreads / kSumRuns;
   red[threadIdx.x] = v;
+  __syncthreads();
+  if (threadIdx.x < kSumRuns) {
+    double s = 0.0;
+#pragma unroll
+    for (int i = 0; i < kRun; ++i) s += red[threadIdx.x * kRun + i];
+    red[kThreads + threadIdx.x] = s;
+  }
   __syncthreads();
   double acc = 0.0;
   if (threadIdx.x == 0)
-    for (int i = 0; i < kThreads; ++i) acc += red[i];
+#pragma unroll
+    for (int i = 0; i < kSumRuns; ++i) acc += red[kThreads + i];
   __syncthreads();
   return acc;
 }
@@ -450,7 +473,7 @@ __device__ __forceinline__ const float* dy_of(const StepArgs& a, int l) {
 
 __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
   __shared__ float part[kWaves * 1024];
-  __shared__ double red[kThreads];
+  __shared__ double red[kThreads + kSumRuns];
   __shared__ int abort_flag;
   const int L = a.layers;
   auto fan_in = [&](int l) { return a.l[l].fan_in; };
@@ -495,11 +518,14 @@ __global__ __launch_bounds__(kThreads) void mlp_step_kernel(StepArgs a) {
           continue;
         }
         r -= n_dx;
-        const int n_dw = tiles64(ly.fan_in, ly.fan_out);
+        const int n_dw = dw_tiles(ly.fan_in, ly.fan_out);
         if (r < n_dw) {  // dW_l = H_l^T dY_l
           Mm j{act_in(a, l), dy, ly.dw, ly.fan_in, ly.fan_out, ly.fan_out, ly.fan_in, ly.fan_out, a.batch, 1, 0, 0,
                0, nullptr, nullptr, 0};
-          mm_tile64(j, r, part);
+          if (dw_small_tiles(ly.fan_in, ly.fan_out))
+            mm_tile(j, r, part);
+          else
+            mm_tile64(j, r, part);
           continue;
         }
         r -= n_dw;
