@@ -2,6 +2,7 @@
 
     python -m paper_1603_04467_amd.profiling trace DIR BENCH_JSON
     python -m paper_1603_04467_amd.profiling traffic FETCH_DIR WRITE_DIR BENCH_JSON
+    python -m paper_1603_04467_amd.profiling phases DIR
 
 DIR, FETCH_DIR and WRITE_DIR are rocprofv3 output directories written with
 `--output-format csv -o run` (run_kernel_stats.csv, run_kernel_trace.csv,
@@ -13,6 +14,9 @@ roofline against it: the dominant kernel's launches are found in the kernel
 trace by their compiled symbol (layout, output type, waves, epilogue) and
 grid, and their mean duration gives the achieved TFLOP/s and the fraction of
 peak, beside the figures bench.py measured with HIP events.
+
+`phases` prints the per-phase kernel times of the fused small step
+(tfd_mlp_step, one launch per phase) found in a kernel trace.
 
 `traffic` prints, per GEMM kernel of the bench line's per-op table, the mean
 FETCH_SIZE and WRITE_SIZE per launch (KiB), each scaled by what the same
@@ -213,11 +217,52 @@ def traffic(fetch_dir: str, write_dir: str, bench_json: str) -> str:
     return "\n".join(out + [""] + recs)
 
 
+def phases(outdir: str, name: str = "mlp_step_kernel") -> str:
+    """Per-phase kernel times of the fused step launched one kernel per phase:
+    the launches of kernel `name` in time order, grouped into steps by the
+    period of their grid sizes (the longest stretch in which every launch has
+    the grid of the launch one period later, taken at the smallest period of
+    at least two with at least three whole steps and more than one distinct
+    grid, which leaves out runs of the one-kernel persistent form); per
+    phase the median duration over the steps, and per step the median span
+    from the first phase's start to the last phase's end."""
+    tr = _rows(os.path.join(outdir, "run_kernel_trace.csv"))
+    ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), int(_grid(r))) for r in tr if name in r["Kernel_Name"])
+    grids = [g for _, _, g in ks]
+    found = None
+    for per in range(2, 17):
+        best, run = (0, 0), 0
+        for i in range(len(grids) - per):
+            run = run + 1 if grids[i] == grids[i + per] else 0
+            if run > best[0]:
+                best = (run, i - run + 1)
+        steps = (best[0] + per) // per
+        if steps >= 3 and len(set(grids[best[1]:best[1] + per])) > 1:
+            found = (per, best[1], steps)
+            break
+    if found is None:
+        return f"no periodic run of {name} launches found"
+    per, s0, steps = found
+    med = lambda v: sorted(v)[len(v) // 2]
+    out = [f"{steps} steps of {per} launches of {name}", "",
+           "| phase | workgroups | median us |", "|---|---|---|"]
+    tot = 0.0
+    for k in range(per):
+        d = [(ks[s0 + k + m * per][1] - ks[s0 + k + m * per][0]) * 1e-3 for m in range(steps)]
+        tot += med(d)
+        out.append(f"| {k} | {grids[s0 + k] // 256} | {med(d):.1f} |")
+    span = [(ks[s0 + m * per + per - 1][1] - ks[s0 + m * per][0]) * 1e-3 for m in range(steps)]
+    out += ["", f"sum of the phase medians {tot:.1f} us; median step span (first start to last end) {med(span):.1f} us"]
+    return "\n".join(out)
+
+
 def main(argv):
     if len(argv) == 3 and argv[0] == "trace":
         print(trace(argv[1], argv[2]))
     elif len(argv) == 4 and argv[0] == "traffic":
         print(traffic(argv[1], argv[2], argv[3]))
+    elif len(argv) == 2 and argv[0] == "phases":
+        print(phases(argv[1]))
     else:
         print(__doc__, file=sys.stderr)
         return 2

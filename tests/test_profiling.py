@@ -117,3 +117,26 @@ def test_traffic_records_round_trip(tmp_path, monkeypatch):
     got = bench.lookup_traffic(TN_ID, "bf16")
     want = 401000.0 * 1024 * 2.0 + 65600.0 * 1024 * 1.0
     assert got is not None and abs(got["bytes"] - want) <= 1e-6 * want
+
+
+def test_phases_groups_the_fused_steps(tmp_path):
+    """Launches of the fused step (3 phases of 4, 2 and 9 workgroups, 5 steps,
+    copies between the steps) followed by persistent launches: the phases
+    are found by the period of the grids, their durations are medians."""
+    rows, t = [], 0
+    for step in range(5):
+        rows.append({"Kernel_Name": COPY, "Grid_Size_X": 1024, "Start_Timestamp": t, "End_Timestamp": t + 500})
+        t += 1000
+        for k, (wg, dur) in enumerate(((4, 3000), (2, 2000), (9, 7000 + step))):
+            rows.append({"Kernel_Name": "tfd::(anonymous namespace)::mlp_step_kernel(StepArgs)", "Grid_Size_X": wg * 256,
+                         "Start_Timestamp": t, "End_Timestamp": t + dur})
+            t += dur + 100
+    for _ in range(4):
+        rows.append({"Kernel_Name": "tfd::(anonymous namespace)::mlp_step_kernel(StepArgs)", "Grid_Size_X": 512 * 256,
+                     "Start_Timestamp": t, "End_Timestamp": t + 40000})
+        t += 41000
+    _write(tmp_path / "run_kernel_trace.csv", rows)
+    out = P.phases(str(tmp_path))
+    assert "5 steps of 3 launches" in out, out
+    assert "| 0 | 4 | 3.0 |" in out and "| 1 | 2 | 2.0 |" in out and "| 2 | 9 | 7.0 |" in out, out
+    assert "sum of the phase medians 12.0 us" in out and "median step span (first start to last end) 12.2 us" in out, out
