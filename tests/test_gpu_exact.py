@@ -15,7 +15,9 @@ wrong epilogue order or a misplaced mask bit changes some of these bits.
 Shapes: the 4096-wide layers' forward and input-gradient MatMuls
 (16384 x 4096 x 4096), their weight gradient (4096 x 4096 x 16384), the tall
 layer's forward (16384 x 32768 x 512) and input gradient (16384 x 512 x 32768,
-split k and not); every layout and every fused epilogue of the kernel.
+split k and not); every layout and every fused epilogue of the kernel; and
+2048 x 2048 x 2112, an odd number (33) of 64-wide k-tiles on the kernel the
+default picks for long k ranges.
 The oracle forms each product once in float64 (section 2, Table 1 MatMul),
 and applies the epilogue ops (BiasAdd, Relu, ReluGrad, BiasAddGrad, the
 squared error) as separate definitions. Every output element is compared,
@@ -44,6 +46,7 @@ SHAPES = {
     (4096, 4096, 16384): 0.125,
     (16384, 32768, 512): 0.5,
     (16384, 512, 32768): 0.0625,
+    (2048, 2048, 2112): 0.34375,   # 33 k-tiles: an odd count on the default long-k kernel
 }
 
 
@@ -154,6 +157,11 @@ for _layout in ("NT", "NN"):
         CASES.append(((16384, 32768, 512), _layout, _epi))
 CASES += [((16384, 512, 32768), "NT", "split"), ((16384, 512, 32768), "NT", "none"),
           ((16384, 512, 32768), "NN", "f32"), ((16384, 512, 32768), "TN", "none")]
+# an odd number of k-tiles (33) where the default picks the scheduled 4-wave
+# loop, which then starts from a stage of zeros
+for _layout in ("NT", "TN"):
+    for _epi in ("none", "relu_mask", "relu_mask_grad", "f32"):
+        CASES.append(((2048, 2048, 2112), _layout, _epi))
 
 
 @pytest.mark.parametrize("shape,layout,epi", CASES, ids=[f"{s[0]}x{s[1]}x{s[2]}-{l}-{e}" for s, l, e in CASES])
