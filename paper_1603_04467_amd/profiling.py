@@ -3,6 +3,7 @@
     python -m paper_1603_04467_amd.profiling trace DIR BENCH_JSON
     python -m paper_1603_04467_amd.profiling traffic FETCH_DIR WRITE_DIR BENCH_JSON
     python -m paper_1603_04467_amd.profiling phases DIR
+    python -m paper_1603_04467_amd.profiling counters PMC_DIR [PMC_DIR ...]
 
 DIR, FETCH_DIR and WRITE_DIR are rocprofv3 output directories written with
 `--output-format csv -o run` (run_kernel_stats.csv, run_kernel_trace.csv,
@@ -17,6 +18,9 @@ peak, beside the figures bench.py measured with HIP events.
 
 `phases` prints the per-phase kernel times of the fused small step
 (tfd_mlp_step, one launch per phase) found in a kernel trace.
+
+`counters` prints the MFMA and LDS counters of the 16-bit GEMM kernels per
+variant from `rocprofv3 --pmc` runs.
 
 `traffic` prints, per GEMM kernel of the bench line's per-op table, the mean
 FETCH_SIZE and WRITE_SIZE per launch (KiB), each scaled by what the same
@@ -256,6 +260,55 @@ def phases(outdir: str, name: str = "mlp_step_kernel") -> str:
     return "\n".join(out)
 
 
+def counters(dirs, flops: float = 2.0 * 16384 * 4096 * 4096) -> str:
+    """MFMA and LDS counters of the 16-bit whole-tile GEMM launches in one or
+    more `rocprofv3 --pmc` output directories (one counter set each), per
+    kernel variant (layout, output type, waves, epilogue), averaged over its
+    launches: duration from the dispatch timestamps; engine clock =
+    GRBM_GUI_ACTIVE / 8 XCDs / duration; TF/s = `flops` / duration; MFMA busy =
+    SQ_VALU_MFMA_BUSY_CYCLES / (clock cycles x 1024 SIMDs); LDS-issue waits =
+    mean SQ_WAIT_INST_LDS / mean SQ_WAVE_CYCLES (from different passes)."""
+    disp, meta = {}, {}
+    for i, d in enumerate(dirs):
+        for r in _rows(os.path.join(d, "run_counter_collection.csv")):
+            f = symbol_fields(r["Kernel_Name"])
+            if f is None:
+                continue
+            lab = (f"{_layout(f)} {f['out']} out, {f['waves'][0] * f['waves'][1]} waves"
+                   + (f", epilogue {_EP_NAME[f['ep']]}" if f["out"] == "bf16" else ""))
+            key = (i, r["Dispatch_Id"])
+            disp.setdefault(key, {})[r["Counter_Name"]] = float(r["Counter_Value"])
+            meta[key] = (lab, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    agg = {}
+    for key, c in disp.items():
+        lab, dur = meta[key]
+        a = agg.setdefault(lab, {})
+        put = lambda k, v: a.setdefault(k, []).append(v)  # noqa: E731
+        cyc = c.get("GRBM_GUI_ACTIVE", float("nan")) / 8.0
+        put("dur", dur * 1e6)
+        put("clock", cyc / dur / 1e9)
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+            put("tflops", flops / dur / 1e12)
+            put("busy", c["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024))
+            put("mfma", c.get("SQ_INSTS_MFMA", float("nan")))
+        for k in ("SQ_WAVE_CYCLES", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS"):
+            if k in c:
+                put(k, c[k])
+    mean = lambda v: sum(v) / len(v) if v else float("nan")  # noqa: E731
+    out = ["| kernel | launches | µs (under counters) | engine clock GHz | TF/s | % of 2516.6 | MFMA busy (of SIMD "
+           "cycles) | MFMA insts | LDS insts | LDS bank-conflict cycles | LDS-issue waits / wave cycles |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for lab in sorted(agg):
+        a = agg[lab]
+        tf = mean(a.get("tflops", []))
+        wl = mean(a.get("SQ_WAIT_INST_LDS", [])) / mean(a.get("SQ_WAVE_CYCLES", []))
+        out.append(f"| {lab} | {len(a.get('busy', []))} | {mean(a['dur']):.0f} | {mean(a['clock']):.2f} | {tf:.0f} | "
+                   f"{100 * tf / 2516.6:.1f} | {100 * mean(a.get('busy', [])):.1f} % | {mean(a.get('mfma', [])):.4g} | "
+                   f"{mean(a.get('SQ_INSTS_LDS', [])):.4g} | {mean(a.get('SQ_LDS_BANK_CONFLICT', [])):.3g} | "
+                   f"{100 * wl:.1f} % |")
+    return "\n".join(out)
+
+
 def main(argv):
     if len(argv) == 3 and argv[0] == "trace":
         print(trace(argv[1], argv[2]))
@@ -263,6 +316,8 @@ def main(argv):
         print(traffic(argv[1], argv[2], argv[3]))
     elif len(argv) == 2 and argv[0] == "phases":
         print(phases(argv[1]))
+    elif len(argv) >= 2 and argv[0] == "counters":
+        print(counters(argv[1:]))
     else:
         print(__doc__, file=sys.stderr)
         return 2

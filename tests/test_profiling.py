@@ -140,3 +140,24 @@ def test_phases_groups_the_fused_steps(tmp_path):
     assert "5 steps of 3 launches" in out, out
     assert "| 0 | 4 | 3.0 |" in out and "| 1 | 2 | 2.0 |" in out and "| 2 | 9 | 7.0 |" in out, out
     assert "sum of the phase medians 12.0 us" in out and "median step span (first start to last end) 12.2 us" in out, out
+
+
+def test_counters_per_variant(tmp_path):
+    """Two counter passes over two launches of one kernel: clock, TF/s, MFMA
+    busy and the LDS-wait share follow from the counters as documented."""
+    d1, d2 = tmp_path / "p1", tmp_path / "p2"
+    d1.mkdir(), d2.mkdir()
+    rows1, rows2 = [], []
+    for disp in (1, 2):
+        base = {"Kernel_Name": TN, "Dispatch_Id": disp, "Start_Timestamp": 0, "End_Timestamp": 400_000}  # 400 us
+        for name, val in (("GRBM_GUI_ACTIVE", 8 * 800_000), ("SQ_VALU_MFMA_BUSY_CYCLES", 0.5 * 800_000 * 1024),
+                          ("SQ_INSTS_MFMA", 100.0), ("SQ_WAVE_CYCLES", 1000.0)):
+            rows1.append(dict(base, Counter_Name=name, Counter_Value=val))
+        for name, val in (("GRBM_GUI_ACTIVE", 8 * 800_000), ("SQ_INSTS_LDS", 7.0), ("SQ_LDS_BANK_CONFLICT", 0.0),
+                          ("SQ_WAIT_INST_LDS", 50.0)):
+            rows2.append(dict(base, Counter_Name=name, Counter_Value=val))
+    _write(d1 / "run_counter_collection.csv", rows1)
+    _write(d2 / "run_counter_collection.csv", rows2)
+    out = P.counters([str(d1), str(d2)], flops=2.0 * 4096 * 4096 * 16384)
+    # 800k cycles in 400 us: 2.00 GHz; 5.5e11 / 400 us = 1374 TF/s; busy 50 %; LDS waits 50 / 1000
+    assert "| TN f32 out, 16 waves | 2 | 400 | 2.00 | 1374 | 54.6 | 50.0 % | 100 | 7 | 0 | 5.0 % |" in out, out
