@@ -22,6 +22,7 @@ from __future__ import annotations
 
 from typing import Optional
 
+import gc
 import numpy as np
 import torch
 
@@ -407,16 +408,30 @@ class DenseStep:
     def capture(self, concurrent=True, num_streams=3):
         """Record one step into a HIP graph (torch.cuda.CUDAGraph); replaying
         it runs the same kernels on the same buffers. The library's calls
-        only launch kernels (no allocation, no memset), so they capture."""
+        only launch kernels (no allocation, no memset), so they capture.
+
+        Python's cyclic garbage collector stays off during the capture, after
+        a collection beforehand: a dead object cycle that holds GPU objects
+        (a step's own HIP graph, events, tensors; DenseStep's launch closures
+        refer back to the step) would otherwise be destroyed in the middle of
+        the capture, and destructors that call the runtime while a stream is
+        being captured abort the process."""
         g = torch.cuda.CUDAGraph()
         if concurrent:
             ex = self.executor(num_streams)
         torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            if concurrent:
-                ex.enqueue(torch.cuda.current_stream())
-            else:
-                self.run()
+        gc.collect()
+        was_enabled = gc.isenabled()
+        gc.disable()
+        try:
+            with torch.cuda.graph(g):
+                if concurrent:
+                    ex.enqueue(torch.cuda.current_stream())
+                else:
+                    self.run()
+        finally:
+            if was_enabled:
+                gc.enable()
         torch.cuda.synchronize()
         return g
 

@@ -8,6 +8,8 @@ Variables, unrelated eager work and a synchronisation, against the eager
 step; the capture contains only the library's kernel launches and the
 executor's event edges (no memset nodes)."""
 
+import gc
+
 import numpy as np
 import pytest
 import torch
@@ -132,3 +134,35 @@ def test_concurrent_and_graph_outputs_match_the_oracle(name, batch, dims, mode):
         _compare_full(w, inp, s)
         check_step(s)
     del g
+
+
+def test_capture_with_dead_steps_holding_graphs():
+    """capture() while dead object cycles hold other steps' HIP graphs and the
+    cyclic collector is set to run at almost every allocation: the steps are
+    collected before the capture, never inside it (a graph destroyed while a
+    stream is being captured aborts the process), and the captured graph
+    replays the eager step bit for bit."""
+    w = workloads.workload("dense784x100")
+    for seed in range(3):
+        dead = DenseStep(w, workloads.generate(w, seed=seed))
+        dead._held = dead.capture(concurrent=False)
+        dead._self = dead                       # a cycle the collector must break
+        del dead
+    old = gc.get_threshold()
+    s = DenseStep(w, workloads.generate(w, seed=5))
+    gc.set_threshold(1, 1, 1)
+    try:
+        graphs = [s.capture(concurrent=False), s.capture(concurrent=True)]
+    finally:
+        gc.set_threshold(*old)
+    s.restore()
+    s.run()
+    torch.cuda.synchronize()
+    want = [t.clone() for t in list(s.h[1:]) + list(s.variables()) + [s.loss]]
+    for g in graphs:
+        s.restore()
+        g.replay()
+        torch.cuda.synchronize()
+        got = list(s.h[1:]) + list(s.variables()) + [s.loss]
+        for a, b in zip(got, want):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
