@@ -383,8 +383,8 @@ class DenseStep:
         """This step's default launch mode: the measured fastest of
         autotune_launch_mode for small steps (run on the first step()), the
         kernels in program order otherwise. On MI355X the small steps pick
-        tfd_mlp_step with one launch per phase: 784x100 0.028 ms (graph replay
-        0.041, program order 0.050), the 784-1024-1024-10 MLP 0.099 ms
+        tfd_mlp_step with one launch per phase: 784x100 0.026 ms (graph replay
+        0.041, program order 0.050), the 784-1024-1024-10 MLP 0.098 ms
         (program order 0.13, graph replay 0.137)."""
         if "_launch_mode" in self.__dict__:
             return self._launch_mode
