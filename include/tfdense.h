@@ -425,8 +425,8 @@ TFD_API tfd_status tfd_convert_bf16_to_f32(const uint16_t* src, float* dst, int6
 TFD_API tfd_status tfd_clock_probe(uint64_t* counters, int64_t iterations, void* stream);
 
 /*
- * One whole training step of a small fp32 multilayer perceptron in a single
- * persistent kernel: the forward pass H_l = Relu(H_{l-1} W_l + b_l) (Figure 1;
+ * One whole training step of a small fp32 multilayer perceptron in one
+ * kernel, launched once per phase or once in all (persistent): the forward pass H_l = Relu(H_{l-1} W_l + b_l) (Figure 1;
  * MatMul, Add and ReLU of section 2, Table 1), the cost head, the gradient
  * subgraph that automatic differentiation adds (section 4.1: ReluGrad, the
  * transposed MatMuls, BiasAddGrad) and the SGD update of the Variables (the
