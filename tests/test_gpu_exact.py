@@ -17,7 +17,8 @@ Shapes: the 4096-wide layers' forward and input-gradient MatMuls
 layer's forward (16384 x 32768 x 512) and input gradient (16384 x 512 x 32768,
 split k and not); every layout and every fused epilogue of the kernel; and
 2048 x 2048 x 2112, an odd number (33) of 64-wide k-tiles on the kernel the
-default picks for long k ranges.
+default picks for long k ranges, and 2048 x 2048 x 12864 with its k range
+split over four workgroups of 51, 51, 51 and 48 k-tiles.
 The oracle forms each product once in float64 (section 2, Table 1 MatMul),
 and applies the epilogue ops (BiasAdd, Relu, ReluGrad, BiasAddGrad, the
 squared error) as separate definitions. Every output element is compared,
@@ -47,6 +48,7 @@ SHAPES = {
     (16384, 32768, 512): 0.5,
     (16384, 512, 32768): 0.0625,
     (2048, 2048, 2112): 0.34375,   # 33 k-tiles: an odd count on the default long-k kernel
+    (2048, 2048, 12864): 0.09375,  # 201 k-tiles over 4 splits of 51, 51, 51 and 48
 }
 
 
@@ -162,6 +164,10 @@ CASES += [((16384, 512, 32768), "NT", "split"), ((16384, 512, 32768), "NT", "non
 for _layout in ("NT", "TN"):
     for _epi in ("none", "relu_mask", "relu_mask_grad", "f32"):
         CASES.append(((2048, 2048, 2112), _layout, _epi))
+# the k range split over 4 workgroups per tile, 51 k-tiles each but the last
+# (48): odd and even counts on the 4-wave loop, partial sums added by the
+# split-k reduction
+CASES += [((2048, 2048, 12864), "NT", "split"), ((2048, 2048, 12864), "TN", "split")]
 
 
 @pytest.mark.parametrize("shape,layout,epi", CASES, ids=[f"{s[0]}x{s[1]}x{s[2]}-{l}-{e}" for s, l, e in CASES])
