@@ -3,9 +3,10 @@
 // training step fused into it.
 //
 // Per workgroup: one 256 x 256 output tile (or one k-range split of it),
-// split over 4 waves of 128 x 128, 8 waves of 128 x 64 (the default for the
-// NN and NT layouts) or 16 waves of 64 x 64 (the default for TN), each wave
-// holding 32 x 32 fragments of v_mfma_f32_32x32x16_bf16 accumulators.
+// split over 4 waves of 128 x 128 (long k ranges; 16 x 16 fragments of
+// v_mfma_f32_16x16x32_bf16 accumulators, brought into the 32 x 32 layout
+// for the epilogue), 8 waves of 128 x 64 or 16 waves of 64 x 64 (32 x 32
+// fragments of v_mfma_f32_32x32x16_bf16 accumulators).
 // The k loop walks 64-wide k-tiles through two LDS stages of 64 KiB:
 //  - global -> LDS copies go straight into LDS (global_load_lds_dwordx4, 1 KiB
 //    per wave instruction), so no registers stage them; the copy of k-tile
@@ -22,7 +23,9 @@
 //  - fragments are double-buffered in registers: the reads for k-step q+1 are
 //    interleaved with the MFMAs of k-step q.
 // K-slot assignment (identical for both operands, so each k is summed once):
-// lane l supplies k = 32*(l/32) + 8*q + e, e = 0..7, in k-step q of a k-tile.
+// with 8 or 16 waves lane l supplies k = 32*(l/32) + 8*q + e, e = 0..7, in
+// k-step q (16 k) of a k-tile; with 4 waves k = 32*q + 8*(l/16) + e in k-step
+// q (32 k).
 // Epilogues (see the EP list below): bias, ReLU and one rounding; a 16-bit
 // tile is staged through LDS and leaves in 16-byte row chunks; ReLU masks
 // from wave ballots; ReluGrad from features or a mask with the tile's column
@@ -80,7 +83,11 @@ struct Params {
 constexpr int kEpPlain = 0, kEpReluGrad = 1, kEpLoss = 2, kEpReluGradBits = 3, kEpMaskOut = 4;
 
 __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
-__device__ __forceinline__ int swz_mn(int krow) { return (krow & 3) << 2; }
+// m/n-contiguous operand: chunk c of k-row kr at slot c ^ swz_mn(kr). Bits 2-3
+// come from kr's low two bits (the four k-rows of one transposing read), bit 1
+// from kr's bit 3: the 4-wave loop's two 16-lane groups of a half-wave read
+// k-rows 8 apart in the same columns, which this puts in different banks.
+__device__ __forceinline__ int swz_mn(int krow) { return ((krow & 3) << 2) | (((krow >> 3) & 1) << 1); }
 
 constexpr int kGroupM = 8;
 __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
@@ -179,34 +186,83 @@ __device__ __forceinline__ void static_for(F&& f) {
     static_for<N, I + 1>(f);
   }
 }
-// 32 x 32 x 16 MFMA, pinned in place by scheduling barriers.
-__device__ __forceinline__ void mfma_acc(f32x16& acc, const u32x4& a, const u32x4& b) {
+// 16 x 16 x 32 MFMA, pinned in place by scheduling barriers. The 4-wave loop
+// uses this form: it does the same work per cycle as the 32 x 32 x 16 form
+// within 6 %, and with half the accumulator traffic per product the chip
+// holds a higher clock under it. It is inline assembly on an accumulator tied
+// to one AGPR quadruple: through the builtin the compiler gives the result
+// registers other than the input's and copies all 256 accumulators back at
+// every loop turn. The compiler then knows nothing of its wait states, so
+// its users keep them: the accumulators are written (zeroed) long before the
+// first MFMA (mfma16_settle), its fragment operands come straight from LDS
+// reads that were waited for, and nothing reads the results before
+// mfma16_settle after the last MFMA.
+__device__ __forceinline__ void mfma16_acc(f32x4& acc, const u32x4& a, const u32x4& b) {
   __builtin_amdgcn_sched_barrier(0);
-  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
-                                               0, 0);
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
   __builtin_amdgcn_sched_barrier(0);
 }
-// Fragment buffer of one operand for one k-step (4 fragments of 32 rows or
-// columns): a k-contiguous operand's fragment is one 16-byte LDS read, an
-// m/n-contiguous one's two 8-byte transposing reads (low and high halves).
+// Wait states between accumulator writes outside the MFMAs and the MFMAs
+// (before the first, after the last): more than the 19 an MFMA of 16 passes
+// needs before another instruction may read its result. Each accumulator is
+// tied to an empty statement after them, so that no read of it can be
+// scheduled before them.
+__device__ __forceinline__ void mfma16_settle(f32x4 (&acc)[8][8]) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 8; ++b) asm volatile("" : "+a"(acc[a][b]));
+}
+// Fragment buffer of one operand for one k-step of the 4-wave loop (8
+// fragments of 16 rows or columns x 32 k): a k-contiguous operand's fragment
+// is one 16-byte LDS read, an m/n-contiguous one's two 8-byte transposing
+// reads (low and high halves).
 template <bool KC> struct FragBuf;
 template <> struct FragBuf<true> {
-  u32x4 f[4];
+  u32x4 f[8];
   template <int I>
   __device__ __forceinline__ u32x4 get() const { return f[I]; }
   // Wait for every outstanding LDS read; tie the registers to the wait so
   // that nothing reads them before their data arrived.
-  __device__ __forceinline__ void tie() { asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3])); }
+  __device__ __forceinline__ void tie() {
+    asm volatile("" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]), "+v"(f[4]), "+v"(f[5]), "+v"(f[6]), "+v"(f[7]));
+  }
 };
 template <> struct FragBuf<false> {
-  u32x2 lo[4], hi[4];
+  u32x2 lo[8], hi[8];
   template <int I>
   __device__ __forceinline__ u32x4 get() const { return u32x4{lo[I].x, lo[I].y, hi[I].x, hi[I].y}; }
   __device__ __forceinline__ void tie() {
-    asm volatile("" : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]),
-                 "+v"(hi[3]));
+    asm volatile("" : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(lo[4]), "+v"(lo[5]), "+v"(lo[6]),
+                 "+v"(lo[7]));
+    asm volatile("" : "+v"(hi[0]), "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]), "+v"(hi[4]), "+v"(hi[5]), "+v"(hi[6]),
+                 "+v"(hi[7]));
   }
 };
+// Accumulators of a 32 x 32 block in the 32 x 32 x 16 MFMA's layout (lane L,
+// register R: column L % 32, row 8 (R / 4) + 4 (L / 32) + R % 4) from its four
+// 16 x 16 blocks x[bi][bj] (rows 16 bi.., columns 16 bj..) in the 16 x 16 x
+// 32 MFMA's layout (lane l, register t: column l % 16, row 4 (l / 16) + t).
+// Per register t and row half bi, a 16-lane row swap then a 32-lane half swap
+// move the four 16-lane rows of x[bi][0] and x[bi][1] into place.
+__device__ __forceinline__ f32x16 acc16_to_32(const f32x4 (&x0)[2], const f32x4 (&x1)[2]) {
+  f32x16 y;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      // (scalar copies: a bit cast of a vector element reads element 0)
+      const float v0 = x0[bi][t], v1 = x1[bi][t];
+      const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v0), __float_as_uint(v1), false, false);
+      const uint32_t p0 = p[0], p1 = p[1];
+      const auto q = __builtin_amdgcn_permlane32_swap(p0, p1, false, false);
+      const uint32_t q0 = q[0], q1 = q[1];
+      y[8 * bi + t] = __uint_as_float(q0);
+      y[8 * bi + 4 + t] = __uint_as_float(q1);
+    }
+  return y;
+}
 template <typename FA, typename FB>
 __device__ __forceinline__ void wait_lds(FA& a, FB& b, bool vm) {
   if (vm)
@@ -355,22 +411,33 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   if constexpr (kWavesM * kWavesN == 4) {
     // One wave per SIMD (128 x 128 wave tiles: 128 KiB of fragment reads per
     // k-tile instead of 192 KiB with 8 waves and 256 KiB with 16), for every
-    // layout. A single wave must keep its matrix core busy, so the schedule is
-    // explicit: in every k-step, the LDS reads of one of the next k-step's
-    // fragments (one read, or the two transposing reads of an m/n-contiguous
-    // operand) after each of the first 8 MFMAs (their latency then hides
-    // behind the last 8), and the copies of the next k-tile spread one pair
-    // per four MFMAs over k-step 3 of the previous k-tile and k-step 0. The
-    // k-tile barrier
-    // sits after k-step 2: by then every wave holds k-step 3's fragments in
-    // registers and its copies of the next k-tile have landed, so k-step 3's
-    // MFMAs run behind the barrier while the next k-tile's first fragments are
-    // read and the copies of the k-tile after it start into the stage just
-    // released. Everything that varies per copy or read is a scalar or an
-    // immediate: copies take a wave-uniform base address (SGPRs) plus a
-    // per-lane 32-bit offset fixed for the whole loop, and the loop is
-    // unrolled over the two LDS stages, whose offsets become immediates.
+    // layout, on 16 x 16 x 32 MFMAs: 8 x 8 accumulator blocks of 16 x 16 per
+    // wave, two k-steps of 32 per k-tile, 64 MFMAs per k-step. A single wave
+    // must keep its matrix core busy, so the schedule is explicit: in every
+    // k-step, the LDS reads of the next k-step's 16 fragments one after every
+    // second MFMA of the first 32 (their latency then hides behind the last
+    // 32), and in k-step 1 the copies of the k-tile after next spread one pair
+    // per eight MFMAs. The k-tile barrier sits between the two k-steps: by
+    // then every wave holds k-step 1's fragments in registers and its copies
+    // of the next k-tile have landed, so k-step 1's MFMAs run behind the
+    // barrier while the next k-tile's first fragments are read and the copies
+    // of the k-tile after it go into the stage just released. Everything that
+    // varies per copy or read is a scalar or an immediate: copies take a
+    // wave-uniform base address (SGPRs) plus a per-lane 32-bit offset fixed
+    // for the whole loop, and the loop is unrolled over the two LDS stages,
+    // whose offsets become immediates.
+    // K-slots: lane l supplies k = 32 q + 8 (l / 16) + e, e = 0..7, in k-step
+    // q of a k-tile (both operands).
     // LDS: A of stage s at s * 32 KiB, B of stage s at 64 KiB + s * 32 KiB.
+    f32x4 acc16[8][8];
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        acc16[a][b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        asm volatile("" : "+a"(acc16[a][b]));
+      }
+    mfma16_settle(acc16);
     const int wv = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform: LDS bases go to M0 directly
     uint32_t offa[8], offb[8];  // per-lane byte offsets of copy instruction j, both operands
 #pragma unroll
@@ -418,97 +485,80 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     // Per-lane LDS read addresses of stage 0; the stage, the k-step and the
     // fragment index enter as immediate offsets where the layout allows.
     // k-contiguous operand (256 rows of 128 B, chunk c of row r at slot
-    // c ^ swz_kc(r)): fragment i of k-step q reads row R + 32 i; rows 64
-    // apart share the swizzle, so an address per (q, i mod 2) and +8 KiB per
-    // two fragments. m/n-contiguous operand (64 k-rows of 512 B): the k-step
-    // and the half of the transposing pair move the k-row by 8 q + 4 s, an
-    // immediate; an address per fragment.
-    const int half = lane >> 5;
-    auto kc_addr = [&](const char* base_lds, int wbase, int q, int par) -> uint32_t {
-      const int r = wbase + par * 32 + (lane & 31);
-      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + r * 128 + (((half * 4 + q) ^ swz_kc(r)) << 4)));
+    // c ^ swz_kc(r)): fragment f of k-step q reads rows R + 16 f + l % 16,
+    // chunk 4 q + l / 16; rows 64 apart share the swizzle, so an address per
+    // (q, f mod 4) and +8 KiB for f >= 4. m/n-contiguous operand (64 k-rows of
+    // 512 B): lane l of 16-lane group g supplies k-row 8 g + (l % 16) / 4 and
+    // four columns 4 (l % 4).. of the fragment's 16; the k-step and the half
+    // of the transposing pair move the k-row by 32 q + 4 h, an immediate (the
+    // swizzle does not see those bits); an address per fragment.
+    const int g16 = lane >> 4, l16 = lane & 15;
+    auto kc_addr = [&](const char* base_lds, int wbase, int q, int f4) -> uint32_t {
+      const int r = wbase + f4 * 16 + l16;
+      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + r * 128 + (((4 * q + g16) ^ swz_kc(r)) << 4)));
     };
-    auto mn_addr = [&](const char* base_lds, int wbase, int j) -> uint32_t {
-      const int g = lane >> 4, lr = lane & 15;
-      const int mn = wbase + j * 32 + 16 * (g & 1) + 4 * (lr & 3);
-      const int kr0 = 32 * half + (lr >> 2);
+    auto mn_addr = [&](const char* base_lds, int wbase, int f) -> uint32_t {
+      const int mn = wbase + f * 16 + 4 * (l16 & 3);
+      const int kr0 = 8 * g16 + (l16 >> 2);
       return (uint32_t)(uintptr_t)((lds_void*)(base_lds + kr0 * 512 + (((mn >> 3) ^ swz_mn(kr0)) << 4) + (mn & 7) * 2));
     };
     uint32_t ra[8], rb[8];
 #pragma unroll
     for (int x = 0; x < 8; ++x) {
-      ra[x] = A_KC ? kc_addr(a_lds(0), wm * kWTM, x >> 1, x & 1) : (x < 4 ? mn_addr(a_lds(0), wm * kWTM, x) : 0u);
-      rb[x] = B_KC ? kc_addr(b_lds(0), wn * kWTN, x >> 1, x & 1) : (x < 4 ? mn_addr(b_lds(0), wn * kWTN, x) : 0u);
+      ra[x] = A_KC ? kc_addr(a_lds(0), wm * kWTM, x >> 2, x & 3) : mn_addr(a_lds(0), wm * kWTM, x);
+      rb[x] = B_KC ? kc_addr(b_lds(0), wn * kWTN, x >> 2, x & 3) : mn_addr(b_lds(0), wn * kWTN, x);
     }
-    // read fragment F (0..3) of an operand, k-step Q of stage S, into a buffer
+    // read fragment F (0..7) of an operand, k-step Q of stage S, into a buffer
     auto read_frag_into = [&](auto f_tag, auto q_tag, auto s_tag, auto& buf, const uint32_t (&ra_)[8]) {
       constexpr int F = decltype(f_tag)::value, Q = decltype(q_tag)::value, S = decltype(s_tag)::value;
       if constexpr (std::is_same<std::decay_t<decltype(buf)>, FragBuf<true>>::value)
-        ds_read_b128_into<(F >> 1) * 8192 + S * kOperandBytes>(buf.f[F], ra_[Q * 2 + (F & 1)]);
+        ds_read_b128_into<(F >> 2) * 8192 + S * kOperandBytes>(buf.f[F], ra_[Q * 4 + (F & 3)]);
       else
-        ds_read_tr_pair_into<(8 * Q) * 512 + S * kOperandBytes, (8 * Q + 4) * 512 + S * kOperandBytes>(
+        ds_read_tr_pair_into<(32 * Q) * 512 + S * kOperandBytes, (32 * Q + 4) * 512 + S * kOperandBytes>(
             buf.lo[F], buf.hi[F], ra_[F]);
     };
     using T_ = std::true_type;
     using F_ = std::false_type;
     FragBuf<A_KC> fa0, fa1;
     FragBuf<B_KC> fb0, fb1;
-    // Read slot r (after MFMA r of a k-step) fills fragment kSlot[r] of A
-    // (< 4) or B (>= 4) for the next k-step. The order keeps at least 6 MFMAs
-    // between an MFMA's last read of a fragment register (A fragment i: MFMA
-    // 4 i + 3 of the previous k-step, B fragment j: MFMA 12 + j) and the LDS
-    // read that overwrites it.
-    // slots: A0, A1, B0, A2, B1, B2, A3, B3
-    // k-step: 16 MFMAs on (fa, fb); after MFMA r < 8 the read of slot r of the
-    // next k-step's fragments (k-step RQ of stage RS; kRead), after MFMAs 0,
-    // 4, 8, 12 one copy pair (kCopy): spread evenly over the k-step, the
-    // copies slow the fragment reads least (measured against pairs after
-    // MFMAs 8-14, 9-15, 1-13 by fours, 2-14, 3-15, 0-6 and 0-3, and against
-    // the A and B copies of a pair two MFMAs apart; the step 4.6 % faster
-    // than with 8-14)
+    // k-step: 64 MFMAs on (fa, fb), A block a = i / 8 by B block b = i % 8.
+    // After MFMA 2 r (r < 16) the read of the next k-step's fragment r (A
+    // 0..7, then B 0..7; k-step RQ of stage RS; kRead): fragment A a was last
+    // read by MFMA 8 a + 7 of the previous k-step and B b by MFMA 56 + b, so
+    // at least 15 MFMAs lie between an MFMA's last read of a fragment register
+    // and the LDS read that overwrites it. After MFMAs 1, 9, .., 57 one copy
+    // pair each (kCopy).
     auto kstep = [&](auto read_tag, auto copy_tag, auto rq_tag, auto rs_tag, auto& fa, auto& fb, auto& na, auto& nb,
-                     const char* ga, const char* gb, int cstage, int cp_half) {
+                     const char* ga, const char* gb, int cstage) {
       constexpr bool kRead = decltype(read_tag)::value, kCopy = decltype(copy_tag)::value;
-      static_for<16>([&](auto i_tag) {
+      static_for<64>([&](auto i_tag) {
         constexpr int i = decltype(i_tag)::value;
-        mfma_acc(acc[i >> 2][i & 3], fa.template get<(i >> 2)>(), fb.template get<(i & 3)>());
-        if constexpr (kRead && i < 8) {
-          constexpr int kSlot[8] = {0, 1, 4, 2, 5, 6, 3, 7};
-          constexpr int sl = kSlot[i];
-          if constexpr (sl < 4)
-            read_frag_into(std::integral_constant<int, sl>{}, rq_tag, rs_tag, na, ra);
+        mfma16_acc(acc16[i >> 3][i & 7], fa.template get<(i >> 3)>(), fb.template get<(i & 7)>());
+        if constexpr (kRead && (i & 1) == 0 && i < 32) {
+          constexpr int r = i >> 1;
+          if constexpr (r < 8)
+            read_frag_into(std::integral_constant<int, r>{}, rq_tag, rs_tag, na, ra);
           else
-            read_frag_into(std::integral_constant<int, sl - 4>{}, rq_tag, rs_tag, nb, rb);
+            read_frag_into(std::integral_constant<int, r - 8>{}, rq_tag, rs_tag, nb, rb);
         }
-        if constexpr (kCopy && (i & 3) == 0) copy_pair(ga, gb, cstage, 4 * cp_half + (i >> 2));
+        if constexpr (kCopy && (i & 7) == 1) copy_pair(ga, gb, cstage, i >> 3);
       });
     };
     using Q0 = std::integral_constant<int, 0>;
     using Q1 = std::integral_constant<int, 1>;
-    using Q2 = std::integral_constant<int, 2>;
-    using Q3 = std::integral_constant<int, 3>;
-    // One k-tile in stage S: copy the second half of the next k-tile in
-    // k-step 0, read the next k-tile's first fragments in k-step 3 and copy
-    // the first half of the one after it there too. Every k-tile runs the
-    // same code, so the loop has no tail: at a join after differently
-    // compiled tails the compiler moves all 256 accumulators between
-    // register files and spills. Past the last k-tile the reads and copies
-    // only touch a stage that no MFMA reads again.
+    // One k-tile in stage S. Every k-tile runs the same code, so the loop has
+    // no tail: at a join after differently compiled tails the compiler moves
+    // all 256 accumulators between register files and spills. Past the last
+    // k-tile the reads and copies only touch a stage that no MFMA reads again.
     auto ktile = [&](auto stage_tag, int kt) {
       constexpr int S = decltype(stage_tag)::value;
       using SN = std::integral_constant<int, 1 - S>;
-      const char* ga1 = abase(kt0 + kt + 1);
-      const char* gb1 = bbase(kt0 + kt + 1);
-      kstep(T_{}, T_{}, Q1{}, stage_tag, fa0, fb0, fa1, fb1, ga1, gb1, 1 - S, 1);
-      wait_lds(fa1, fb1, false);
-      kstep(T_{}, F_{}, Q2{}, stage_tag, fa1, fb1, fa0, fb0, ga1, gb1, 1 - S, 0);
-      wait_lds(fa0, fb0, false);
-      kstep(T_{}, F_{}, Q3{}, stage_tag, fa0, fb0, fa1, fb1, ga1, gb1, 1 - S, 0);
-      // the k-tile barrier: k-step 3's fragments are in registers, this
+      kstep(T_{}, F_{}, Q1{}, stage_tag, fa0, fb0, fa1, fb1, nullptr, nullptr, 0);
+      // the k-tile barrier: k-step 1's fragments are in registers, this
       // wave's copies of the next k-tile have landed
       wait_lds(fa1, fb1, true);
       __builtin_amdgcn_s_barrier();
-      kstep(T_{}, T_{}, Q0{}, SN{}, fa1, fb1, fa0, fb0, abase(kt0 + kt + 2), bbase(kt0 + kt + 2), S, 0);
+      kstep(T_{}, T_{}, Q0{}, SN{}, fa1, fb1, fa0, fb0, abase(kt0 + kt + 2), bbase(kt0 + kt + 2), S);
       // The next k-tile's first fragments are waited for here, at the end of
       // the k-tile and not at the start of the next: no read is in flight
       // across a branch, where the compiler may move registers around.
@@ -519,8 +569,8 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     // Two k-tiles per trip, stage 0 then stage 1. An odd count starts at
     // k-tile -1: stage 0 filled with zeros, whose products add exact zeros.
     int kt = (kt_count & 1) ? -1 : 0;
-    // prologue: k-tile kt in stage 0, its first fragments, and the first half
-    // of k-tile kt + 1's copies into stage 1
+    // prologue: k-tile kt in stage 0, its first fragments, and k-tile kt + 1's
+    // copies into stage 1
     if (kt == 0) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) copy_pair(abase(kt0), bbase(kt0), 0, j);
@@ -534,18 +584,28 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     }
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
-    static_for<4>([&](auto f_tag) {
+    static_for<8>([&](auto f_tag) {
       read_frag_into(f_tag, Q0{}, S0{}, fa0, ra);
       read_frag_into(f_tag, Q0{}, S0{}, fb0, rb);
     });
 #pragma unroll
-    for (int j = 0; j < 4; ++j) copy_pair(abase(kt0 + kt + 1), bbase(kt0 + kt + 1), 1, j);
+    for (int j = 0; j < 8; ++j) copy_pair(abase(kt0 + kt + 1), bbase(kt0 + kt + 1), 1, j);
     wait_lds(fa0, fb0, false);
     for (; kt < kt_count; kt += 2) {
       ktile(S0{}, kt);
       ktile(S1{}, kt + 1);
     }
     __builtin_amdgcn_s_waitcnt(0);
+    mfma16_settle(acc16);
+    // into the 32 x 32 accumulator layout the epilogue takes
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 x0[2] = {acc16[2 * i][2 * j], acc16[2 * i + 1][2 * j]};
+        const f32x4 x1[2] = {acc16[2 * i][2 * j + 1], acc16[2 * i + 1][2 * j + 1]};
+        acc[i][j] = acc16_to_32(x0, x1);
+      }
   } else {
   copy_tile<A_KC, kThreads>(p.a, p.lda, m0, kt0 * kBK, smem, wave, lane);
   copy_tile<B_KC, kThreads>(p.b, p.ldb, n0, kt0 * kBK, smem + kOperandBytes, wave, lane);
