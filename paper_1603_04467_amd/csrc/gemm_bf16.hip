@@ -1035,17 +1035,16 @@ hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // A is k-contiguous unless transposed; B is k-contiguous when transposed.
   // Defaults measured inside the training step (4096-wide layers, batch
   // 16384; 512 -> 32768 layer): the scheduled 4-wave loop (one wave per SIMD,
-  // 128 x 128 wave tiles) for long k ranges: NT forward with mask 0.465 vs
-  // 0.480 ms with 8 waves, NT input gradient with ReluGrad 0.463 vs 0.476,
-  // TN weight gradient 0.405 vs 0.445 with 16 waves. With 8 k-tiles or fewer
+  // 128 x 128 wave tiles, 16 x 16 x 32 MFMAs) for long k ranges: NT forward
+  // with mask 0.433 vs 0.480 ms with 8 waves, the squared-error output layer
+  // 0.510 vs 0.520, NT input gradient with ReluGrad 0.430 vs 0.476, TN
+  // weight gradient 0.365 vs 0.445 with 16 waves. With 8 k-tiles or fewer
   // per workgroup the epilogue dominates and 2 waves per SIMD overlap it
-  // better (512 -> 32768 forward 0.65 vs 0.70 ms); the squared-error
-  // epilogue, whose target chunks 8 waves prefetch during the staging, also
-  // keeps 8 waves (0.52 vs 0.54 ms). NN keeps 8 waves.
+  // better (512 -> 32768 forward 0.64 vs 0.76 ms). NN keeps 8 waves.
   const int64_t kt = d.splits > 1 ? d.kt_per : d.k / kBK;
   const bool long_k = kt >= 32;
   if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, 8), s);
-  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, long_k && !d.target ? 4 : 8), s);
+  if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, long_k ? 4 : 8), s);
   return launch_gemm_bf16_256_tn(d, s);
 }
 #endif
