@@ -24,8 +24,8 @@
 //    interleaved with the MFMAs of k-step q.
 // K-slot assignment (identical for both operands, so each k is summed once):
 // with 8 or 16 waves lane l supplies k = 32*(l/32) + 8*q + e, e = 0..7, in
-// k-step q (16 k) of a k-tile; with 4 waves k = 32*q + 8*(l/16) + e in k-step
-// q (32 k).
+// k-step q (16 k) of a k-tile; with 4 waves k = 32*q + 8*c(l/16) + e in k-step
+// q (32 k), c = 0, 2, 1, 3.
 // Epilogues (see the EP list below): bias, ReLU and one rounding; a 16-bit
 // tile is staged through LDS and leaves in 16-byte row chunks; ReLU masks
 // from wave ballots; ReluGrad from features or a mask with the tile's column
@@ -85,9 +85,9 @@ constexpr int kEpPlain = 0, kEpReluGrad = 1, kEpLoss = 2, kEpReluGradBits = 3, k
 __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; }
 // m/n-contiguous operand: chunk c of k-row kr at slot c ^ swz_mn(kr). Bits 2-3
 // come from kr's low two bits (the four k-rows of one transposing read), bit 1
-// from kr's bit 3: the 4-wave loop's two 16-lane groups of a half-wave read
-// k-rows 8 apart in the same columns, which this puts in different banks.
-__device__ __forceinline__ int swz_mn(int krow) { return ((krow & 3) << 2) | (((krow >> 3) & 1) << 1); }
+// from kr's bit 4: the 4-wave loop's two 16-lane groups of a half-wave read
+// k-rows 16 apart in the same columns, which this puts in different banks.
+__device__ __forceinline__ int swz_mn(int krow) { return ((krow & 3) << 2) | (((krow >> 4) & 1) << 1); }
 
 constexpr int kGroupM = 8;
 __device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
@@ -426,8 +426,11 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     // wave-uniform base address (SGPRs) plus a per-lane 32-bit offset fixed
     // for the whole loop, and the loop is unrolled over the two LDS stages,
     // whose offsets become immediates.
-    // K-slots: lane l supplies k = 32 q + 8 (l / 16) + e, e = 0..7, in k-step
-    // q of a k-tile (both operands).
+    // K-slots: lane l of 16-lane group g = l / 16 supplies k = 32 q + 8 c(g)
+    // + e, e = 0..7, in k-step q of a k-tile (both operands), c(g) = 0, 2, 1, 3:
+    // the two groups of a half-wave, whose LDS reads are served together, then
+    // read 16-byte chunks two apart of the same rows (k-contiguous operand) or
+    // k-rows 16 apart (m/n-contiguous), which puts them in different banks.
     // LDS: A of stage s at s * 32 KiB, B of stage s at 64 KiB + s * 32 KiB.
     f32x4 acc16[8][8];
 #pragma unroll
@@ -486,20 +489,21 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     // fragment index enter as immediate offsets where the layout allows.
     // k-contiguous operand (256 rows of 128 B, chunk c of row r at slot
     // c ^ swz_kc(r)): fragment f of k-step q reads rows R + 16 f + l % 16,
-    // chunk 4 q + l / 16; rows 64 apart share the swizzle, so an address per
+    // chunk 4 q + c(g); rows 64 apart share the swizzle, so an address per
     // (q, f mod 4) and +8 KiB for f >= 4. m/n-contiguous operand (64 k-rows of
-    // 512 B): lane l of 16-lane group g supplies k-row 8 g + (l % 16) / 4 and
-    // four columns 4 (l % 4).. of the fragment's 16; the k-step and the half
-    // of the transposing pair move the k-row by 32 q + 4 h, an immediate (the
-    // swizzle does not see those bits); an address per fragment.
+    // 512 B): lane l of 16-lane group g supplies k-row 8 c(g) + (l % 16) / 4
+    // and four columns 4 (l % 4).. of the fragment's 16; the k-step and the
+    // half of the transposing pair move the k-row by 32 q + 4 h, an immediate
+    // (the swizzle does not see those bits); an address per fragment.
     const int g16 = lane >> 4, l16 = lane & 15;
+    const int cg = ((g16 & 1) << 1) | (g16 >> 1);  // c(g)
     auto kc_addr = [&](const char* base_lds, int wbase, int q, int f4) -> uint32_t {
       const int r = wbase + f4 * 16 + l16;
-      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + r * 128 + (((4 * q + g16) ^ swz_kc(r)) << 4)));
+      return (uint32_t)(uintptr_t)((lds_void*)(base_lds + r * 128 + (((4 * q + cg) ^ swz_kc(r)) << 4)));
     };
     auto mn_addr = [&](const char* base_lds, int wbase, int f) -> uint32_t {
       const int mn = wbase + f * 16 + 4 * (l16 & 3);
-      const int kr0 = 8 * g16 + (l16 >> 2);
+      const int kr0 = 8 * cg + (l16 >> 2);
       return (uint32_t)(uintptr_t)((lds_void*)(base_lds + kr0 * 512 + (((mn >> 3) ^ swz_mn(kr0)) << 4) + (mn & 7) * 2));
     };
     uint32_t ra[8], rb[8];
