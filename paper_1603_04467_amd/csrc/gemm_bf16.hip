@@ -525,25 +525,25 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     using F_ = std::false_type;
     FragBuf<A_KC> fa0, fa1;
     FragBuf<B_KC> fb0, fb1;
-    // k-step: 64 MFMAs on (fa, fb), A block a = i / 8 by B block b = i % 8.
-    // After MFMA 2 r (r < 16) the read of the next k-step's fragment r (A
-    // 0..7, then B 0..7; k-step RQ of stage RS; kRead): fragment A a was last
-    // read by MFMA 8 a + 7 of the previous k-step and B b by MFMA 56 + b, so
-    // at least 15 MFMAs lie between an MFMA's last read of a fragment register
-    // and the LDS read that overwrites it. After MFMAs 1, 9, .., 57 one copy
-    // pair each (kCopy).
+    // k-step: 64 MFMAs on (fa, fb), A block a = i % 8 by B block b = i / 8
+    // (0.3 % faster in the step than the A-major order). After MFMA 2 r
+    // (r < 16) the read of the next k-step's fragment r (B 0..7, then A 0..7;
+    // k-step RQ of stage RS; kRead): fragment B b was last read by MFMA 8 b + 7
+    // of the previous k-step and A a by MFMA 56 + a, so at least 15 MFMAs lie
+    // between an MFMA's last read of a fragment register and the LDS read that
+    // overwrites it. After MFMAs 1, 9, .., 57 one copy pair each (kCopy).
     auto kstep = [&](auto read_tag, auto copy_tag, auto rq_tag, auto rs_tag, auto& fa, auto& fb, auto& na, auto& nb,
                      const char* ga, const char* gb, int cstage) {
       constexpr bool kRead = decltype(read_tag)::value, kCopy = decltype(copy_tag)::value;
       static_for<64>([&](auto i_tag) {
         constexpr int i = decltype(i_tag)::value;
-        mfma16_acc(acc16[i >> 3][i & 7], fa.template get<(i >> 3)>(), fb.template get<(i & 7)>());
+        mfma16_acc(acc16[i & 7][i >> 3], fa.template get<(i & 7)>(), fb.template get<(i >> 3)>());
         if constexpr (kRead && (i & 1) == 0 && i < 32) {
           constexpr int r = i >> 1;
           if constexpr (r < 8)
-            read_frag_into(std::integral_constant<int, r>{}, rq_tag, rs_tag, na, ra);
+            read_frag_into(std::integral_constant<int, r>{}, rq_tag, rs_tag, nb, rb);
           else
-            read_frag_into(std::integral_constant<int, r - 8>{}, rq_tag, rs_tag, nb, rb);
+            read_frag_into(std::integral_constant<int, r - 8>{}, rq_tag, rs_tag, na, ra);
         }
         if constexpr (kCopy && (i & 7) == 1) copy_pair(ga, gb, cstage, i >> 3);
       });
