@@ -387,9 +387,10 @@ TFD_API tfd_status tfd_apply_gradient_descent(float* var, float alpha, const flo
  * the updated weights in the same pass:
  *   var_bf16  (nullable): rows x cols, var_bf16[r * cols + c]   = bf16(var[r, c]),
  *   var_bf16_t (nullable): cols x rows, var_bf16_t[c * rows + r] = bf16(var[r, c]).
- * The transposed copy lets the forward MatMul read the weights k-contiguous
+ * The transposed copy lets a forward MatMul read the weights k-contiguous
  * (transpose_b = 1) while the input-gradient MatMul reads the untransposed
- * copy. None of the four buffers may overlap another.
+ * copy (the step keeps it for layers with fan_in under 2048). None of the
+ * four buffers may overlap another.
  */
 TFD_API tfd_status tfd_apply_gradient_descent_matrix(float* var, float alpha, const float* delta,
                                              int64_t rows, int64_t cols, uint16_t* var_bf16,

@@ -1044,10 +1044,11 @@ hipError_t launch_gemm_bf16_256(const GemmDesc& d, hipStream_t s) {
   // 0.510 vs 0.520, NT input gradient with ReluGrad 0.430 vs 0.476, TN
   // weight gradient 0.365 vs 0.445 with 16 waves. With 8 k-tiles or fewer
   // per workgroup the epilogue dominates and 2 waves per SIMD overlap it
-  // better (512 -> 32768 forward 0.64 vs 0.76 ms). NN keeps 8 waves.
+  // better (512 -> 32768 forward 0.64 vs 0.76 ms). NN the same way: the
+  // 4096-wide forward on W (B m/n-contiguous) 0.414-0.436 ms on 4 waves.
   const int64_t kt = d.splits > 1 ? d.kt_per : d.k / kBK;
   const bool long_k = kt >= 32;
-  if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, 8), s);
+  if (!d.ta && !d.tb) return launch_waves<true, false>(d, waves_for(kTuneBf16WavesNN, long_k ? 4 : 8), s);
   if (!d.ta && d.tb) return launch_waves<true, true>(d, waves_for(kTuneBf16WavesNT, long_k ? 4 : 8), s);
   return launch_gemm_bf16_256_tn(d, s);
 }

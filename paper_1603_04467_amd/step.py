@@ -111,13 +111,18 @@ class DenseStep:
         self.weights = [_to_device(a, w.act, dev) for a in inputs["weights"]]
         self.masters = None if inputs["masters"] is None else [_to_device(a, "f32", dev) for a in inputs["masters"]]
         self.biases = [_to_device(a, "f32", dev) for a in inputs["biases"]]
-        # With fp32 masters, the 16-bit weights are kept twice: W [fan_in, fan_out]
-        # for the input-gradient MatMul and W^T [fan_out, fan_in] so that the
-        # forward MatMul reads its weight operand k-contiguous (transpose_b).
-        # Both copies are refreshed by the update kernel. 16-bit weights that
-        # are never updated (a given layer) get the same transposed copy once.
+        # 16-bit weights over a short k range (a layer with fan_in under 2048,
+        # whose forward MatMul runs the 8-wave kernel) are kept twice: W
+        # [fan_in, fan_out] for the input-gradient MatMul and W^T [fan_out,
+        # fan_in] so that the forward MatMul reads its weight operand
+        # k-contiguous (transpose_b). With fp32 masters both copies are
+        # refreshed by the update kernel; weights that are never updated (a
+        # given layer) get the transposed copy once. Over long k ranges the
+        # forward reads W itself (the 4-wave kernel is as fast on it), and the
+        # update writes one 16-bit copy instead of two.
         self.weights_t = None
-        if self.masters is not None or (w.act == "bf16" and not w.update):
+        short_k = w.act == "bf16" and min(w.dims[:-1]) < 2048
+        if short_k and (self.masters is not None or not w.update):
             self.weights_t = [torch.empty(w.dims[l + 1], w.dims[l], dtype=self.act, device=dev) for l in range(L)]
         # layout of the forward MatMul ("NN": H W; "NT": H (W^T)^T)
         self.forward_layout = "NT" if self.weights_t is not None else "NN"
@@ -147,15 +152,17 @@ class DenseStep:
                  for l in range(L)]
         self.workspace = torch.empty(max(need), dtype=torch.uint8, device=dev)
 
-        if self.weights_t is not None:
-            # derive W^T with the update kernel (alpha = 0) from the masters, or
-            # from the exact fp32 value of the 16-bit W (which it reproduces bit
-            # for bit)
+        if self.weights_t is not None or self.masters is not None:
+            # derive the 16-bit W (and W^T) with the update kernel (alpha = 0)
+            # from the masters under the workload's rounding, or W^T from the
+            # exact fp32 value of a given 16-bit W (which it reproduces bit for
+            # bit)
             for l in range(L):
                 self.dw[l].zero_()
                 if self.masters is not None:
-                    T.tfd_apply_gradient_descent_matrix(self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
-                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding)
+                    T.tfd_apply_gradient_descent_matrix(
+                        self.masters[l], 0.0, self.dw[l], var_bf16=self.weights[l],
+                        var_bf16_t=None if self.weights_t is None else self.weights_t[l], rounding=w.rounding)
                 else:
                     wf = torch.empty(w.dims[l], w.dims[l + 1], dtype=torch.float32, device=dev)
                     T.tfd_convert_bf16_to_f32(self.weights[l], wf)
@@ -259,7 +266,8 @@ class DenseStep:
             def sgd(st):
                 if self.masters is not None:
                     T.tfd_apply_gradient_descent_matrix(self.masters[l], w.lr, self.dw[l], var_bf16=self.weights[l],
-                                                        var_bf16_t=self.weights_t[l], rounding=w.rounding, stream=st)
+                                                        var_bf16_t=None if self.weights_t is None else self.weights_t[l],
+                                                        rounding=w.rounding, stream=st)
                 else:
                     T.tfd_apply_gradient_descent(self.weights[l], w.lr, self.dw[l], stream=st)
                 T.tfd_apply_gradient_descent(self.biases[l], w.lr, self.db[l], stream=st)
