@@ -77,6 +77,7 @@ struct Params {
   // its fp32 partial tile to c + s * m * ldc; the partials are summed by
   // splitk_reduce_kernel.
   int splits, kt_per;
+  int group_m;  // tile-rows per band of the tile order (tile_of_block)
 };
 
 // Epilogues of the whole-tile kernel beyond bias/ReLU (16-bit outputs only).
@@ -89,15 +90,17 @@ __device__ __forceinline__ int swz_kc(int row) { return (row ^ (row >> 3)) & 7; 
 // k-rows 16 apart in the same columns, which this puts in different banks.
 __device__ __forceinline__ int swz_mn(int krow) { return ((krow & 3) << 2) | (((krow >> 4) & 1) << 1); }
 
-constexpr int kGroupM = 8;
-__device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+// Block -> tile: the blocks dispatched to one XCD (every eighth) take a
+// contiguous range of tiles, walked in bands of group_m tile-rows, so that the
+// tiles an XCD runs at a time share operand panels in its L2.
+__device__ __forceinline__ void tile_of_block(int bid, int tiles_m, int tiles_n, int group_m, int& tm, int& tn) {
   const int total = tiles_m * tiles_n;
   int t = bid;
   if (total % kNumXcd == 0) t = (bid % kNumXcd) * (total / kNumXcd) + bid / kNumXcd;
-  const int per_group = kGroupM * tiles_n;
+  const int per_group = group_m * tiles_n;
   const int group = t / per_group;
-  const int first_m = group * kGroupM;
-  const int gsize = min(tiles_m - first_m, kGroupM);
+  const int first_m = group * group_m;
+  const int gsize = min(tiles_m - first_m, group_m);
   const int in_group = t - group * per_group;
   tm = first_m + in_group % gsize;
   tn = in_group / gsize;
@@ -366,7 +369,7 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
     split = bid / tiles;
     bid -= split * tiles;
   }
-  tile_of_block(bid, p.tiles_m, p.tiles_n, tm, tn);
+  tile_of_block(bid, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
   if constexpr (kMaskLds) {
     // one dword per lane: instruction j of a wave covers rows 8 b .. 8 b + 7
@@ -921,6 +924,10 @@ hipError_t launch(const GemmDesc& d, hipStream_t s) {
   p.ldm = d.ldm;
   p.splits = d.splits > 1 ? d.splits : 1;
   p.kt_per = p.splits > 1 ? (int)d.kt_per : p.k / kBK;
+  // bands of 8 tile-rows; 4 for the unsplit 4-wave NT products (the input
+  // gradients of the 4096-wide step: 0.416 vs 0.423 ms inside it, while the
+  // NN forward and TN weight gradients are fastest with 8)
+  p.group_m = (A_KC && B_KC && WM * WN == 4 && p.splits == 1) ? 4 : 8;
   dim3 grid(p.tiles_m * p.tiles_n * p.splits), block(64 * WM * WN);
   if (p.splits > 1)  // fp32 partial tiles, plain (the reduction applies the epilogue)
     hipLaunchKernelGGL((gemm_bf16_256<A_KC, B_KC, float, WM, WN>), grid, block, 0, s, p);
