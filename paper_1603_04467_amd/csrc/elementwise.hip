@@ -309,6 +309,10 @@ __global__ __launch_bounds__(kThreads) void sgd_matrix_kernel(float* __restrict_
 
 hipError_t launch_sgd_matrix(float* var, float alpha, const float* delta, int64_t rows, int64_t cols,
                              uint16_t* shadow, uint16_t* shadow_t, bool trunc, hipStream_t s) {
+  // without the transposed copy the matrix is one contiguous array: the
+  // element-wise update (whole 1 KiB per wave instruction) does the same
+  // arithmetic per element
+  if (!shadow_t) return launch_sgd(var, alpha, delta, rows * cols, shadow, trunc, s);
   const bool vec = aligned16(var) && aligned16(delta) && cols % 4 == 0 &&
                    ((reinterpret_cast<uintptr_t>(shadow) & 7) == 0) && aligned16(shadow_t);
   dim3 grid((unsigned)((cols + kSgdTile - 1) / kSgdTile), (unsigned)((rows + kSgdTile - 1) / kSgdTile));
