@@ -353,9 +353,10 @@ __global__ __launch_bounds__(64 * kWavesM * kWavesN) void gemm_bf16_256(Params p
   constexpr int kThreads = 64 * kWavesM * kWavesN;
   constexpr int kFM = kBM / kWavesM / 32, kFN = kBN / kWavesN / 32;  // fragments per wave
   __shared__ __attribute__((aligned(1024))) char smem[2 * kStageBytes];
-  // With 4 waves the accumulators fill all 256 AGPRs and the epilogue has no
-  // registers to prefetch into: the ReluGrad mask words of the tile (256 rows
-  // x 8 words) are copied into LDS of their own with the first k-tile.
+  // With 4 waves the accumulators fill all 256 AGPRs and the k loop's
+  // fragments most of the VGPRs, so nothing is prefetched into registers
+  // before the loop: the ReluGrad mask words of the tile (256 rows x 8 words)
+  // are copied into LDS of their own with the first k-tile.
   constexpr bool kMaskLds = EP == kEpReluGradBits && kWavesM * kWavesN == 4;
   __shared__ uint32_t mask_lds[kMaskLds ? kBM * (kBN / 32) : 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
